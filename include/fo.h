@@ -1,0 +1,302 @@
+/*
+ * fo.h -- C ABI of the signaled + reordered GEMM path (FlashOverlap,
+ * "Efficient and Adaptable Overlapping for Computation and Communication via
+ * Signaling and Reordering") for AMD Instinct MI355X (gfx950).
+ *
+ * The path, one GPU:
+ *
+ *   1. fo_plan_groups          host: tile dispatch order, waves, wave groups,
+ *                              the reorder map and the per-group segments
+ *                              (Sections 3.2-3.4, Algorithm 1).
+ *   2. fo_gemm_signal_reorder  GPU, stream 1: C = A x B whose epilogue stores
+ *                              every finished tile into its group-contiguous
+ *                              slot and then bumps the group's counter
+ *                              (Section 3.2 Approach, Section 3.3 Approach,
+ *                              Section 5).
+ *   3. fo_consume_group        GPU, stream 2: waits until a group's counter
+ *                              reaches the group's tile count, then processes
+ *                              the group's contiguous (ptr, len) segment. On
+ *                              one GPU this stands in for the collective
+ *                              (Section 3.3 Motivation: one library call per
+ *                              contiguous buffer).
+ *   4. fo_post_reorder         GPU: restores row-major order, fused with bias
+ *                              add and RMSNorm (Section 3.3 Approach, last
+ *                              paragraph; Section 6.6).
+ *
+ * Conventions for every call:
+ *   - Device buffers are plain device pointers owned by the caller. The
+ *     library never allocates, frees or retains device memory.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Launches are asynchronous; no call synchronizes the device.
+ *   - Every call returns fo_status and never aborts. On failure nothing is
+ *     launched and fo_last_error() returns a message for the calling thread.
+ *   - fp16 is IEEE binary16, bf16 is bfloat16; both are stored as 16-bit
+ *     words. Accumulation is fp32 (MFMA); results are rounded to nearest-even.
+ */
+#ifndef FO_H_
+#define FO_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FO_OK = 0,
+    FO_ERR_ARG = -1,          /* null / inconsistent argument            */
+    FO_ERR_SHAPE = -2,        /* a dimension does not fit the tiling      */
+    FO_ERR_UNSUPPORTED = -3,  /* no kernel for this dtype / tile / pattern */
+    FO_ERR_HIP = -4,          /* a HIP runtime call failed                */
+    FO_ERR_TIMEOUT = -5       /* reported through a status word only      */
+} fo_status;
+
+typedef enum { FO_FP16 = 0, FO_BF16 = 1 } fo_dtype;
+
+/* Pre-communication reorder pattern (Section 3.3, Approach (1)-(3)). */
+typedef enum {
+    FO_PATTERN_TILE = 0,      /* AllReduce: tiles, column-of-tiles buffer          */
+    FO_PATTERN_SUBTILE = 1,   /* ReduceScatter: each tile cut into R row slices     */
+    FO_PATTERN_SUBTOKEN = 2,  /* All-to-All: tile rows into per-destination pools   */
+    FO_PATTERN_ROWMAJOR = 3   /* plain GEMM output (no reorder)                     */
+} fo_pattern;
+
+/* Dispatch order of tiles (Section 2.1.2, block swizzling). Workgroup p of
+ * the GEMM grid computes tile order(p); tiles are numbered row-major over
+ * the (M/tile_m) x (N/tile_n) tile grid.
+ *   ROWMAJOR: order(p) = p.
+ *   GROUPED:  bands of `group_m` tile rows; inside a band the position walks
+ *             down a column of the band, then to the next column:
+ *               band = q / (group_m*tiles_n), first = band*group_m,
+ *               rows = min(tiles_m - first, group_m), r = q % (group_m*tiles_n),
+ *               tm = first + r % rows, tn = r / rows          (q = p).
+ *   XCD:      position p runs on chiplet x = p % num_xcds; chiplet x's
+ *             positions take a contiguous share of the GROUPED order:
+ *               per = ceil(tiles/num_xcds), full = tiles % num_xcds (or
+ *               num_xcds when 0), l = p / num_xcds,
+ *               q = x < full ? x*per + l : full*per + (x-full)*(per-1) + l,
+ *             then GROUPED on q. On MI355X (8 chiplets of 32 CUs, each with
+ *             its own L2) and group_m = 4 a chiplet's 32 concurrent 256x128
+ *             tiles form a 4x8 block: 1024 rows of A, 1024 columns of B. */
+typedef enum { FO_ORDER_ROWMAJOR = 0, FO_ORDER_GROUPED = 1, FO_ORDER_XCD = 2 } fo_order;
+
+/* Unit of a wave-group partition (Section 3.2 Insight: a group is >= 1 whole
+ * waves; TILES allows tile-wise signalling inside one wave). */
+typedef enum { FO_UNIT_WAVES = 0, FO_UNIT_TILES = 1 } fo_unit;
+
+/* The GEMM and its decomposition. Host memory, read during the call only. */
+typedef struct {
+    int64_t M, N, K;          /* C[M,N] = A[M,K] x B[K,N] (Section 2.1.1)          */
+    int32_t dtype;            /* fo_dtype of A, B, C                                */
+    int32_t tile_m, tile_n;   /* output tile; kernels exist for 256x128 and 64x64   */
+    int32_t order;            /* fo_order                                           */
+    int32_t group_m;          /* band height for GROUPED / XCD (>= 1)               */
+    int32_t num_xcds;         /* chiplets for XCD (>= 1)                            */
+    int32_t num_cus;          /* compute units of the device (256 on MI355X)        */
+    int32_t wg_per_cu;        /* GEMM workgroups resident per CU (1 here)           */
+    int32_t reserved_cus;     /* CUs left to communication (Algorithm 1)            */
+    int32_t pattern;          /* fo_pattern                                         */
+    int32_t num_dest;         /* R for SUBTILE (divides tile_m), B for SUBTOKEN    */
+    const int32_t* dest_perm; /* SUBTILE: [R], slice k goes to buffer dest_perm[k];
+                                 NULL = identity. Must be a permutation.            */
+    const int32_t* row_bucket;/* SUBTOKEN: [M], destination of every row, in [0,B) */
+} fo_problem;
+
+/* How the waves are grouped (Section 3.4; Section 4 for the search). */
+typedef struct {
+    int32_t unit;             /* fo_unit of `sizes`                                 */
+    int32_t num_groups;       /* > 0: explicit `sizes`; 0: Algorithm 1 search       */
+    const int32_t* sizes;     /* [num_groups], each >= 1, summing to T waves (or to
+                                 the tile count when unit == TILES)                 */
+    double gemm_us;           /* search: measured GEMM duration                     */
+    const double* curve_bytes;/* search: sampled communication latency curve,      */
+    const double* curve_us;   /*   ascending bytes; piecewise-linear in between,    */
+    int32_t curve_len;        /*   end-point bandwidth outside the samples          */
+    int32_t s_first, s_last;  /* search pruning |G_1| <= s_first, |G_P| <= s_last
+                                 (Section 4.1 uses 2 and 4); <= 0 means no bound    */
+} fo_grouping;
+
+typedef struct fo_plan fo_plan;   /* opaque, library-owned host memory */
+
+/*
+ * fo_plan_groups -- build the plan (host only, deterministic, no GPU work).
+ *
+ * Tiles: tiles = (M/tile_m)(N/tile_n). Waves (Section 2.1.1; Algorithm 1's
+ * wave count): W = (num_cus - reserved_cus) * wg_per_cu tiles run together; the
+ * tile at dispatch position p runs in wave p / W; T = ceil(tiles / W).
+ * Slots (Section 3.3 Approach (1)): the slot of a tile is its dispatch
+ * position, so earlier waves come first and a wave's tiles are adjacent.
+ * Groups: group j owns slots [first_j, first_{j+1}); with unit WAVES
+ * first_j = min(W * (waves before j), tiles). Counter target of group j =
+ * first_{j+1} - first_j (Section 3.2: the j-th count fires at |G_j| tiles).
+ * With num_groups == 0 the partition is Algorithm 1: every partition of T
+ * waves (cut vector x = 0 .. 2^(T-1)-1, bit i = cut after wave i+1, T <= 24)
+ * that meets the pruning bounds is scored by the predicted overlapped
+ * latency, and the first strictly smallest wins.
+ *
+ * Errors: FO_ERR_ARG (null pointers, sizes that do not sum, bad enum,
+ * missing dest_perm/row_bucket data, bad curve), FO_ERR_SHAPE (M % tile_m,
+ * N % tile_n, tile_m % R not zero, negative dims), FO_ERR_UNSUPPORTED
+ * (search with T > 24). *out is set only on FO_OK; free with fo_plan_destroy.
+ */
+fo_status fo_plan_groups(const fo_problem* problem, const fo_grouping* grouping, fo_plan** out);
+void fo_plan_destroy(fo_plan* plan);
+
+/* Plan accessors. Arrays stay valid until fo_plan_destroy. */
+int32_t fo_plan_num_tiles(const fo_plan* plan);
+int32_t fo_plan_wave_width(const fo_plan* plan);      /* W                        */
+int32_t fo_plan_num_waves(const fo_plan* plan);       /* T                        */
+int32_t fo_plan_num_groups(const fo_plan* plan);      /* P                        */
+const int32_t* fo_plan_group_sizes(const fo_plan* plan);   /* [P], in the plan's unit */
+const int32_t* fo_plan_order(const fo_plan* plan);         /* [tiles] position -> tile */
+const int32_t* fo_plan_tile_to_slot(const fo_plan* plan);  /* [tiles] the reorder map  */
+const int32_t* fo_plan_group_first(const fo_plan* plan);   /* [P+1] first slot          */
+const int32_t* fo_plan_group_targets(const fo_plan* plan); /* [P] tiles = final count   */
+double fo_plan_predicted_us(const fo_plan* plan);     /* Algorithm 1 estimate (0 if
+                                                         the partition was given)   */
+/* SUBTOKEN pools: pool_base[(s * B) + b] = subtokens of pool b in slots < s,
+ * s in [0, tiles]; pool_off[b] = first subtoken of pool b, b in [0, B]. */
+const int32_t* fo_plan_pool_base(const fo_plan* plan);
+const int32_t* fo_plan_pool_off(const fo_plan* plan);
+
+/*
+ * Communication segments, in the order a caller issues them: entry e is
+ * seg[5e .. 5e+4] = {group j, destination d, src_off, dst_off, len}, in
+ * elements. Source = the GEMM output buffer (and the peer partial, laid out
+ * the same way); destination = the consumer's buffer of
+ * fo_plan_dest_elems() elements.
+ *   TILE:     one segment per group: its slots, dst_off = src_off.
+ *   SUBTILE:  one per (group j, slice k): h = tile_m/R rows of each of the
+ *             group's n_j tiles; src_off = first_j*tile_m*tile_n + k*n_j*h*tile_n;
+ *             destination buffer dest_perm[k] (buffers of tiles*h*tile_n
+ *             elements laid end to end) at rows first_j*h.
+ *   SUBTOKEN: one per (group, pool b); the receive buffer mirrors the pools.
+ *   ROWMAJOR: one segment, the whole output, for the last group.
+ */
+int32_t fo_plan_num_segments(const fo_plan* plan);
+const int64_t* fo_plan_segments(const fo_plan* plan);
+int64_t fo_plan_dest_elems(const fo_plan* plan);
+
+/*
+ * Device image of the plan's tables (int32 words): what the GEMM epilogue
+ * and the post-reorder kernel read. fo_plan_to_device copies it into a
+ * caller-owned device buffer of at least fo_plan_device_bytes() bytes
+ * (16-byte aligned) on `stream` (asynchronous when the copy engine allows;
+ * the host plan must stay alive until the copy is complete).
+ */
+size_t fo_plan_device_bytes(const fo_plan* plan);
+fo_status fo_plan_to_device(const fo_plan* plan, void* dev_buf, size_t bytes, void* stream);
+
+/*
+ * fo_gemm_signal_reorder -- C = A x B with the reordering, signalling
+ * epilogue (Section 3.2 Approach; Section 3.3 Approach; Section 5: the
+ * reorder sits in the epilogue, the main loop is untouched).
+ *
+ * A: [M, K] row-major. W: B^T, [N, K] row-major (K contiguous, the weight
+ * layout of a linear layer). K must be a multiple of 64; A, W, C_out 16-byte
+ * aligned. C_out by pattern:
+ *   ROWMAJOR: [M, N] row-major.
+ *   TILE:     [tiles*tile_m, tile_n] row-major; slot s holds the tile at rows
+ *             [s*tile_m, (s+1)*tile_m).
+ *   SUBTILE:  M*N elements, group j at [first_j*tile_m*tile_n, ...) laid out
+ *             [R][n_j][h][tile_n]: slice k of the group's i-th slot at
+ *             first_j*tile_m*tile_n + (k*n_j + i)*h*tile_n.
+ *   SUBTOKEN: M*N elements, pool b at pool_off[b]*tile_n; row r of tile
+ *             (tm, tn) in slot s goes to subtoken pool_off[b] +
+ *             pool_base[s*B+b] + (rank of row r among rows of tile row tm
+ *             bound for b), b = row_bucket[tm*tile_m + r].
+ * counters: [P] uint32, zeroed by the caller before the launch and before any
+ * consumer of this run starts (see fo_reset_counters); NULL = no signalling.
+ * When a tile's stores are complete, one workgroup-level agent-scope
+ * release increment is made on counters[group of its slot]; when the GEMM
+ * is done, counters[j] == target_j for every j.
+ * dev_plan: the plan's device image (fo_plan_to_device).
+ * Errors: FO_ERR_ARG, FO_ERR_SHAPE (K % 64), FO_ERR_UNSUPPORTED (tile shape
+ * other than 256x128 / 64x64), FO_ERR_HIP (launch failure).
+ */
+fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan,
+                                 const void* A, const void* W, void* C_out,
+                                 uint32_t* counters, void* stream);
+
+/*
+ * fo_consume_group -- the communication stand-in for one contiguous segment
+ * (Section 5: a signalling kernel holds the communication of a group until
+ * the group's count reaches its size; the communication itself only sees a
+ * contiguous buffer).
+ *
+ * Waits until *counter >= target (agent-scope acquire), then for i < len:
+ *   peer != NULL:  dst[i] = RNE(src[i] + peer[i])   (AllReduce/ReduceScatter
+ *                  of this GPU's partial with one peer partial)
+ *   peer == NULL:  dst[i] = src[i]                  (All-to-All copy)
+ * counter == NULL: no wait. The wait is bounded (fo_set_poll_timeout_us); on
+ * timeout the segment is not written and *status_word (if non-NULL, device
+ * uint32, caller-zeroed) gets bit 0 set. Buffers must not overlap. Any
+ * alignment works; 16-byte-aligned pointers take the vector path.
+ * Errors: FO_ERR_ARG (null src/dst with len > 0, len < 0, bad dtype).
+ */
+fo_status fo_consume_group(const void* src, const void* peer, void* dst, int64_t len,
+                           int32_t dtype, const uint32_t* counter, uint32_t target,
+                           uint32_t* status_word, void* stream);
+
+/*
+ * fo_post_reorder -- post-communication reorder fused into the following
+ * element-wise op (Section 3.3: loads go by the reordered index; Section 6.6
+ * measures it fused with RMSNorm).
+ *
+ * src: the consumer's destination buffer (fo_plan_dest_elems elements).
+ * out: [M, N] row-major, x[i, n] = src[position of (i, n)].
+ * Then, row-wise: h = x + bias (bias [N] or NULL), and if do_rmsnorm:
+ * y = h / sqrt(mean_n(h^2) + eps) * gamma (gamma [N] or NULL = 1), in fp32,
+ * rounded once to the dtype; else y = h.
+ * Errors: FO_ERR_ARG, FO_ERR_UNSUPPORTED (N % 8 or tile_n % 8 not zero),
+ * FO_ERR_HIP.
+ */
+fo_status fo_post_reorder(const fo_plan* plan, const void* dev_plan, const void* src,
+                          void* out, const void* bias, const void* gamma, float eps,
+                          int32_t do_rmsnorm, void* stream);
+
+/* ---- orchestration and helpers ----------------------------------------- */
+
+/* Zero n counters with a fill kernel (safe inside captured graphs). */
+fo_status fo_reset_counters(uint32_t* counters, int32_t n, void* stream);
+
+/*
+ * One overlapped run of the whole path (Section 5: GEMM on one stream, the
+ * signalling + communication on another; Figure 5 order):
+ *   gemm_stream: reset counters + status -> event E0 -> GEMM (signalling)
+ *   comm_stream: wait E0 -> fo_consume_group for every plan segment -> event E1
+ *   gemm_stream: wait E1 -> fo_post_reorder (if out != NULL)
+ * With comm_stream == gemm_stream (or NULL) the same work runs serialized.
+ * Buffers: C_out (GEMM output, see fo_gemm_signal_reorder), peer (NULL for
+ * All-to-All; else the peer's partial in C_out's layout), dst
+ * (fo_plan_dest_elems), out ([M, N] or NULL), counters [P], status_word [1].
+ * gemm_begin_event / gemm_end_event: optional caller-owned hipEvent_t (as
+ * void*) recorded on gemm_stream right before and after the GEMM launch, so
+ * a caller can time the GEMM inside the overlapped run; NULL = none.
+ * Uses two library-owned HIP events per calling thread and device.
+ */
+fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan,
+                            const void* A, const void* W, void* C_out,
+                            const void* peer, void* dst, void* out,
+                            const void* bias, const void* gamma, float eps,
+                            int32_t do_rmsnorm, uint32_t* counters,
+                            uint32_t* status_word, void* gemm_stream, void* comm_stream,
+                            void* gemm_begin_event, void* gemm_end_event);
+
+/* Upper bound of one consumer wait, in microseconds (default 2 s; env
+ * FO_POLL_TIMEOUT_US overrides at load time). */
+void fo_set_poll_timeout_us(int64_t us);
+int64_t fo_get_poll_timeout_us(void);
+
+/* Compute units of HIP device `device` (for fo_problem.num_cus). */
+fo_status fo_device_num_cus(int32_t device, int32_t* num_cus);
+
+const char* fo_status_string(fo_status status);
+const char* fo_last_error(void);   /* thread-local; "" when none */
+
+#ifdef __cplusplus
+}  /* extern "C" */
+#endif
+
+#endif  /* FO_H_ */

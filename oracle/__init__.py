@@ -221,7 +221,7 @@ def dispatch_order(tiles_m: int, tiles_n: int, order: str,
 
 
 # --------------------------------------------------------------------------
-# Waves and wave groups (Sections 2.1.1, 3.2, 3.4; Algorithm 1 line 3)
+# Waves and wave groups (Sections 2.1.1, 3.2, 3.4; Algorithm 1 wave count)
 # --------------------------------------------------------------------------
 
 def wave_width(num_cus: int, wg_per_cu: int = 1, reserved_cus: int = 0) -> int:
@@ -283,7 +283,7 @@ def all_partitions(T: int) -> List[Tuple[int, ...]]:
 
 
 def candidates(T: int, s_first: int, s_last: int) -> List[Tuple[int, ...]]:
-    """Algorithm 1 line 7 with the Section 4.1 pruning |G_1| <= S_1 and
+    """Algorithm 1 candidate generation with the Section 4.1 pruning |G_1| <= S_1 and
     |G_P| <= S_P."""
     return [g for g in all_partitions(T) if g[0] <= s_first and g[-1] <= s_last]
 
@@ -310,7 +310,7 @@ def interp_latency(curve_bytes: Sequence[float], curve_us: Sequence[float], nbyt
 
 def predicted_latency(sizes: Sequence[int], T: int, gemm_us: float,
                       comm_us_of_group: Callable[[int], float]) -> float:
-    """Algorithm 1 lines 9-17 for one candidate.
+    """Algorithm 1 latency prediction for one candidate.
 
     For each group G_i in order: the communication of the previous group
     starts when both the computation so far and the previous communication

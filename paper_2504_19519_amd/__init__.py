@@ -1,0 +1,315 @@
+"""Python binding of libfo, the MI355X (gfx950) signaled + reordered GEMM path.
+
+Argument marshalling only: every step of the path runs in the HIP kernels of
+``libfo.so`` (see ``include/fo.h`` for the contract of each call). Device
+buffers are passed as raw device pointers (ints) or as objects with a
+``data_ptr()`` method (e.g. torch tensors on a ROCm device); streams as raw
+hipStream_t handles or objects with a ``cuda_stream`` attribute.
+
+The library must be built (``python -m paper_2504_19519_amd.build``); there is
+no fallback path: importing the binding without the library raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+__all__ = [
+    "FoError", "Plan", "plan_groups", "gemm_signal_reorder", "consume_group",
+    "post_reorder", "reset_counters", "run_overlapped", "set_poll_timeout_us",
+    "get_poll_timeout_us", "device_num_cus", "LIB_PATH",
+    "FP16", "BF16", "TILE", "SUBTILE", "SUBTOKEN", "ROWMAJOR",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfo.so")
+
+FP16, BF16 = 0, 1
+TILE, SUBTILE, SUBTOKEN, ROWMAJOR = 0, 1, 2, 3
+ORDER_ROWMAJOR, ORDER_GROUPED, ORDER_XCD = 0, 1, 2
+UNIT_WAVES, UNIT_TILES = 0, 1
+
+_DTYPES = {"fp16": FP16, "bf16": BF16, FP16: FP16, BF16: BF16}
+_PATTERNS = {"tile": TILE, "subtile": SUBTILE, "subtoken": SUBTOKEN, "rowmajor": ROWMAJOR,
+             TILE: TILE, SUBTILE: SUBTILE, SUBTOKEN: SUBTOKEN, ROWMAJOR: ROWMAJOR}
+_ORDERS = {"rowmajor": ORDER_ROWMAJOR, "grouped": ORDER_GROUPED, "xcd": ORDER_XCD,
+           ORDER_ROWMAJOR: ORDER_ROWMAJOR, ORDER_GROUPED: ORDER_GROUPED, ORDER_XCD: ORDER_XCD}
+_UNITS = {"waves": UNIT_WAVES, "tiles": UNIT_TILES, UNIT_WAVES: UNIT_WAVES, UNIT_TILES: UNIT_TILES}
+
+
+class FoError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"libfo status {status}: {message}")
+        self.status = status
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
+                ("dtype", ctypes.c_int32), ("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32),
+                ("order", ctypes.c_int32), ("group_m", ctypes.c_int32), ("num_xcds", ctypes.c_int32),
+                ("num_cus", ctypes.c_int32), ("wg_per_cu", ctypes.c_int32),
+                ("reserved_cus", ctypes.c_int32), ("pattern", ctypes.c_int32),
+                ("num_dest", ctypes.c_int32),
+                ("dest_perm", ctypes.POINTER(ctypes.c_int32)),
+                ("row_bucket", ctypes.POINTER(ctypes.c_int32))]
+
+
+class _Grouping(ctypes.Structure):
+    _fields_ = [("unit", ctypes.c_int32), ("num_groups", ctypes.c_int32),
+                ("sizes", ctypes.POINTER(ctypes.c_int32)), ("gemm_us", ctypes.c_double),
+                ("curve_bytes", ctypes.POINTER(ctypes.c_double)),
+                ("curve_us", ctypes.POINTER(ctypes.c_double)), ("curve_len", ctypes.c_int32),
+                ("s_first", ctypes.c_int32), ("s_last", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libfo.so. Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          f"`python -m paper_2504_19519_amd.build` (no fallback path exists)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, u32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32
+    pi32 = ctypes.POINTER(ctypes.c_int32)
+    pi64 = ctypes.POINTER(ctypes.c_int64)
+    L.fo_plan_groups.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Grouping), ctypes.POINTER(vp)]
+    L.fo_plan_destroy.argtypes = [vp]
+    for name in ("num_tiles", "wave_width", "num_waves", "num_groups", "num_segments"):
+        f = getattr(L, f"fo_plan_{name}")
+        f.argtypes, f.restype = [vp], i32
+    for name in ("group_sizes", "order", "tile_to_slot", "group_first", "group_targets",
+                 "pool_base", "pool_off"):
+        f = getattr(L, f"fo_plan_{name}")
+        f.argtypes, f.restype = [vp], pi32
+    L.fo_plan_segments.argtypes, L.fo_plan_segments.restype = [vp], pi64
+    L.fo_plan_dest_elems.argtypes, L.fo_plan_dest_elems.restype = [vp], i64
+    L.fo_plan_predicted_us.argtypes, L.fo_plan_predicted_us.restype = [vp], ctypes.c_double
+    L.fo_plan_device_bytes.argtypes, L.fo_plan_device_bytes.restype = [vp], ctypes.c_size_t
+    L.fo_plan_to_device.argtypes = [vp, vp, ctypes.c_size_t, vp]
+    L.fo_gemm_signal_reorder.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+    L.fo_consume_group.argtypes = [vp, vp, vp, i64, i32, vp, u32, vp, vp]
+    L.fo_post_reorder.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_float, i32, vp]
+    L.fo_reset_counters.argtypes = [vp, i32, vp]
+    L.fo_run_overlapped.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, i32,
+                                    vp, vp, vp, vp, vp, vp]
+    L.fo_set_poll_timeout_us.argtypes = [i64]
+    L.fo_get_poll_timeout_us.restype = i64
+    L.fo_device_num_cus.argtypes = [i32, pi32]
+    L.fo_status_string.argtypes, L.fo_status_string.restype = [ctypes.c_int], ctypes.c_char_p
+    L.fo_last_error.restype = ctypes.c_char_p
+    for f in (L.fo_plan_groups, L.fo_plan_to_device, L.fo_gemm_signal_reorder, L.fo_consume_group,
+              L.fo_post_reorder, L.fo_reset_counters, L.fo_run_overlapped, L.fo_device_num_cus):
+        f.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        L = lib()
+        msg = L.fo_last_error().decode() or L.fo_status_string(status).decode()
+        raise FoError(status, msg)
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, (int, np.integer)):
+        return int(x) or None
+    if hasattr(x, "data_ptr"):
+        return int(x.data_ptr())
+    raise TypeError(f"cannot take a device pointer of {type(x)}")
+
+
+def _stream(s) -> Optional[int]:
+    if s is None:
+        return None
+    if isinstance(s, (int, np.integer)):
+        return int(s) or None
+    if hasattr(s, "cuda_stream"):
+        return int(s.cuda_stream) or None
+    raise TypeError(f"cannot take a stream handle of {type(s)}")
+
+
+def _event(e) -> Optional[int]:
+    if e is None:
+        return None
+    if isinstance(e, (int, np.integer)):
+        return int(e) or None
+    if hasattr(e, "cuda_event"):
+        h = int(e.cuda_event)
+        if not h:
+            raise ValueError("event not created yet: record it once before passing it")
+        return h
+    raise TypeError(f"cannot take an event handle of {type(e)}")
+
+
+def _i32_array(values) -> Optional[ctypes.Array]:
+    if values is None:
+        return None
+    a = np.ascontiguousarray(np.asarray(values, dtype=np.int32))
+    return (ctypes.c_int32 * a.size).from_buffer_copy(a.tobytes()) if a.size else (ctypes.c_int32 * 1)()
+
+
+def _f64_array(values) -> Optional[ctypes.Array]:
+    if values is None:
+        return None
+    a = np.ascontiguousarray(np.asarray(values, dtype=np.float64))
+    return (ctypes.c_double * a.size).from_buffer_copy(a.tobytes())
+
+
+class Plan:
+    """Owner of an fo_plan (host memory); arrays are copied out as numpy."""
+
+    def __init__(self, handle: int, M: int, N: int, K: int, dtype: int, tile_m: int, tile_n: int,
+                 pattern: int, num_dest: int):
+        self._h = ctypes.c_void_p(handle)
+        self.M, self.N, self.K, self.dtype = M, N, K, dtype
+        self.tile_m, self.tile_n, self.pattern, self.num_dest = tile_m, tile_n, pattern, num_dest
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.fo_plan_destroy(h)
+            self._h = None
+
+    @property
+    def handle(self) -> ctypes.c_void_p:
+        return self._h
+
+    def _arr(self, fn, n, dtype=np.int32):
+        if n <= 0:
+            return np.zeros(0, dtype=dtype)
+        p = fn(self._h)
+        return np.ctypeslib.as_array(p, shape=(n,)).copy()
+
+    @property
+    def tiles(self) -> int: return lib().fo_plan_num_tiles(self._h)
+    @property
+    def W(self) -> int: return lib().fo_plan_wave_width(self._h)
+    @property
+    def T(self) -> int: return lib().fo_plan_num_waves(self._h)
+    @property
+    def P(self) -> int: return lib().fo_plan_num_groups(self._h)
+    @property
+    def sizes(self) -> np.ndarray: return self._arr(lib().fo_plan_group_sizes, self.P)
+    @property
+    def order(self) -> np.ndarray: return self._arr(lib().fo_plan_order, self.tiles)
+    @property
+    def tile_to_slot(self) -> np.ndarray: return self._arr(lib().fo_plan_tile_to_slot, self.tiles)
+    @property
+    def group_first(self) -> np.ndarray: return self._arr(lib().fo_plan_group_first, self.P + 1)
+    @property
+    def targets(self) -> np.ndarray: return self._arr(lib().fo_plan_group_targets, self.P)
+    @property
+    def predicted_us(self) -> float: return lib().fo_plan_predicted_us(self._h)
+    @property
+    def dest_elems(self) -> int: return lib().fo_plan_dest_elems(self._h)
+    @property
+    def device_bytes(self) -> int: return lib().fo_plan_device_bytes(self._h)
+
+    @property
+    def segments(self) -> np.ndarray:
+        n = lib().fo_plan_num_segments(self._h)
+        return self._arr(lib().fo_plan_segments, 5 * n, np.int64).reshape(n, 5)
+
+    @property
+    def pool_base(self) -> Optional[np.ndarray]:
+        if self.pattern != SUBTOKEN:
+            return None
+        return self._arr(lib().fo_plan_pool_base, (self.tiles + 1) * self.num_dest).reshape(
+            self.tiles + 1, self.num_dest)
+
+    @property
+    def pool_off(self) -> Optional[np.ndarray]:
+        if self.pattern != SUBTOKEN:
+            return None
+        return self._arr(lib().fo_plan_pool_off, self.num_dest + 1)
+
+    def to_device(self, dev_buf, nbytes: Optional[int] = None, stream=None) -> None:
+        nb = self.device_bytes if nbytes is None else nbytes
+        _check(lib().fo_plan_to_device(self._h, _ptr(dev_buf), nb, _stream(stream)))
+
+
+def plan_groups(M: int, N: int, K: int, *, dtype="fp16", tile_m: int = 256, tile_n: int = 128,
+                order="xcd", group_m: int = 4, num_xcds: int = 8, num_cus: int = 256,
+                wg_per_cu: int = 1, reserved_cus: int = 0, pattern="tile", num_dest: int = 0,
+                dest_perm: Optional[Sequence[int]] = None, row_bucket=None,
+                sizes: Optional[Sequence[int]] = None, unit="waves", gemm_us: float = 0.0,
+                curve_bytes=None, curve_us=None, s_first: int = 2, s_last: int = 4) -> Plan:
+    """fo_plan_groups: sizes=None runs the Algorithm 1 search (needs gemm_us
+    and the latency curve)."""
+    L = lib()
+    perm = _i32_array(dest_perm)
+    buck = _i32_array(row_bucket)
+    prob = _Problem(M=M, N=N, K=K, dtype=_DTYPES[dtype], tile_m=tile_m, tile_n=tile_n,
+                    order=_ORDERS[order], group_m=group_m, num_xcds=num_xcds, num_cus=num_cus,
+                    wg_per_cu=wg_per_cu, reserved_cus=reserved_cus, pattern=_PATTERNS[pattern],
+                    num_dest=num_dest,
+                    dest_perm=ctypes.cast(perm, ctypes.POINTER(ctypes.c_int32)) if perm is not None else None,
+                    row_bucket=ctypes.cast(buck, ctypes.POINTER(ctypes.c_int32)) if buck is not None else None)
+    sz = _i32_array(sizes)
+    cb, cu = _f64_array(curve_bytes), _f64_array(curve_us)
+    grp = _Grouping(unit=_UNITS[unit], num_groups=0 if sizes is None else len(sizes),
+                    sizes=ctypes.cast(sz, ctypes.POINTER(ctypes.c_int32)) if sz is not None else None,
+                    gemm_us=gemm_us,
+                    curve_bytes=ctypes.cast(cb, ctypes.POINTER(ctypes.c_double)) if cb is not None else None,
+                    curve_us=ctypes.cast(cu, ctypes.POINTER(ctypes.c_double)) if cu is not None else None,
+                    curve_len=0 if curve_bytes is None else len(curve_bytes),
+                    s_first=s_first, s_last=s_last)
+    out = ctypes.c_void_p()
+    _check(L.fo_plan_groups(ctypes.byref(prob), ctypes.byref(grp), ctypes.byref(out)))
+    return Plan(out.value, M, N, K, _DTYPES[dtype], tile_m, tile_n, _PATTERNS[pattern], num_dest)
+
+
+def gemm_signal_reorder(plan: Plan, dev_plan, A, W, C_out, counters=None, stream=None) -> None:
+    _check(lib().fo_gemm_signal_reorder(plan.handle, _ptr(dev_plan), _ptr(A), _ptr(W), _ptr(C_out),
+                                        _ptr(counters), _stream(stream)))
+
+
+def consume_group(src, peer, dst, length: int, dtype, counter=None, target: int = 0,
+                  status_word=None, stream=None) -> None:
+    _check(lib().fo_consume_group(_ptr(src), _ptr(peer), _ptr(dst), int(length), _DTYPES[dtype],
+                                  _ptr(counter), int(target), _ptr(status_word), _stream(stream)))
+
+
+def post_reorder(plan: Plan, dev_plan, src, out, bias=None, gamma=None, eps: float = 1e-6,
+                 do_rmsnorm: bool = False, stream=None) -> None:
+    _check(lib().fo_post_reorder(plan.handle, _ptr(dev_plan), _ptr(src), _ptr(out), _ptr(bias),
+                                 _ptr(gamma), float(eps), int(bool(do_rmsnorm)), _stream(stream)))
+
+
+def reset_counters(counters, n: int, stream=None) -> None:
+    _check(lib().fo_reset_counters(_ptr(counters), int(n), _stream(stream)))
+
+
+def run_overlapped(plan: Plan, dev_plan, A, W, C_out, peer, dst, out=None, bias=None, gamma=None,
+                   eps: float = 1e-6, do_rmsnorm: bool = False, counters=None, status_word=None,
+                   gemm_stream=None, comm_stream=None, gemm_begin_event=None,
+                   gemm_end_event=None) -> None:
+    _check(lib().fo_run_overlapped(plan.handle, _ptr(dev_plan), _ptr(A), _ptr(W), _ptr(C_out),
+                                   _ptr(peer), _ptr(dst), _ptr(out), _ptr(bias), _ptr(gamma),
+                                   float(eps), int(bool(do_rmsnorm)), _ptr(counters),
+                                   _ptr(status_word), _stream(gemm_stream), _stream(comm_stream),
+                                   _event(gemm_begin_event), _event(gemm_end_event)))
+
+
+def set_poll_timeout_us(us: int) -> None:
+    lib().fo_set_poll_timeout_us(int(us))
+
+
+def get_poll_timeout_us() -> int:
+    return int(lib().fo_get_poll_timeout_us())
+
+
+def device_num_cus(device: int = 0) -> int:
+    v = ctypes.c_int32()
+    _check(lib().fo_device_num_cus(device, ctypes.byref(v)))
+    return int(v.value)

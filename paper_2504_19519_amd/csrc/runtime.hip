@@ -1,0 +1,295 @@
+// C ABI entry points of libfo: argument checks, device-plan addressing,
+// kernel launches and the two-stream orchestration of one overlapped run.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+
+#include "consume.h"
+#include "fo_internal.h"
+#include "gemm.h"
+#include "post.h"
+
+namespace fo {
+
+namespace {
+thread_local std::string t_last_error;
+std::atomic<int64_t> g_timeout_us{[] {
+    const char* e = std::getenv("FO_POLL_TIMEOUT_US");
+    if (e && *e) {
+        char* end = nullptr;
+        const long long v = std::strtoll(e, &end, 10);
+        if (end && *end == '\0' && v > 0) return (int64_t)v;
+    }
+    return (int64_t)2000000;
+}()};
+
+constexpr int kMaxDevices = 64;
+std::atomic<int64_t> g_clock_khz[kMaxDevices];   // 0 = unknown
+
+fo_status hip_fail(const char* what, hipError_t e) {
+    return fail(FO_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// Ticks of the device wall clock (s_memrealtime) per microsecond x 1000.
+fo_status clock_khz(int64_t* out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail("hipGetDevice", e);
+    if (dev < 0 || dev >= kMaxDevices) return fail(FO_ERR_ARG, "device index out of range");
+    int64_t k = g_clock_khz[dev].load(std::memory_order_relaxed);
+    if (k == 0) {
+        int rate = 0;
+        e = hipDeviceGetAttribute(&rate, hipDeviceAttributeWallClockRate, dev);
+        if (e != hipSuccess || rate <= 0) rate = 100000;   // 100 MHz constant clock
+        k = rate;
+        g_clock_khz[dev].store(k, std::memory_order_relaxed);
+    }
+    *out = k;
+    return FO_OK;
+}
+
+__global__ void fill_u32_kernel(uint32_t* p, int32_t n, uint32_t v) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+template <typename T>
+const T* dev_table(const void* dev_plan, int64_t word_off) {
+    if (word_off < 0) return nullptr;
+    return reinterpret_cast<const T*>(static_cast<const int32_t*>(dev_plan) + word_off);
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+}  // namespace
+
+fo_status fail(fo_status st, const std::string& msg) {
+    t_last_error = msg;
+    return st;
+}
+void clear_error() { t_last_error.clear(); }
+int64_t poll_timeout_us() { return g_timeout_us.load(std::memory_order_relaxed); }
+
+}  // namespace fo
+
+extern "C" {
+
+const char* fo_status_string(fo_status s) {
+    switch (s) {
+        case FO_OK: return "ok";
+        case FO_ERR_ARG: return "invalid argument";
+        case FO_ERR_SHAPE: return "shape does not fit the tiling";
+        case FO_ERR_UNSUPPORTED: return "unsupported configuration";
+        case FO_ERR_HIP: return "HIP runtime error";
+        case FO_ERR_TIMEOUT: return "consumer wait timed out";
+    }
+    return "unknown status";
+}
+
+const char* fo_last_error(void) { return fo::t_last_error.c_str(); }
+
+void fo_set_poll_timeout_us(int64_t us) {
+    if (us > 0) fo::g_timeout_us.store(us, std::memory_order_relaxed);
+}
+int64_t fo_get_poll_timeout_us(void) { return fo::poll_timeout_us(); }
+
+fo_status fo_device_num_cus(int32_t device, int32_t* num_cus) {
+    fo::clear_error();
+    if (!num_cus) return fo::fail(FO_ERR_ARG, "num_cus is NULL");
+    int v = 0;
+    hipError_t e = hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, device);
+    if (e != hipSuccess) return fo::hip_fail("hipDeviceGetAttribute", e);
+    *num_cus = v;
+    return FO_OK;
+}
+
+fo_status fo_reset_counters(uint32_t* counters, int32_t n, void* stream) {
+    fo::clear_error();
+    if (n < 0 || (n > 0 && !counters)) return fo::fail(FO_ERR_ARG, "bad counters");
+    if (n == 0) return FO_OK;
+    hipLaunchKernelGGL(fo::fill_u32_kernel, dim3((n + 255) / 256), dim3(256), 0,
+                       (hipStream_t)stream, counters, n, 0u);
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? FO_OK : fo::hip_fail("fill kernel launch", e);
+}
+
+fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan, const void* A,
+                                 const void* W, void* C_out, uint32_t* counters, void* stream) {
+    fo::clear_error();
+    if (!plan) return fo::fail(FO_ERR_ARG, "plan is NULL");
+    if (plan->tiles == 0) return FO_OK;
+    if (!A || !W || !C_out) return fo::fail(FO_ERR_ARG, "null operand");
+    if (!dev_plan && (plan->pattern != FO_PATTERN_ROWMAJOR || counters))
+        return fo::fail(FO_ERR_ARG, "dev_plan is NULL");
+    if (!fo::gemm_tile_supported(plan->tile_m, plan->tile_n))
+        return fo::fail(FO_ERR_UNSUPPORTED, "GEMM kernels exist for 256x128 and 64x64 tiles");
+    if (plan->K % 64) return fo::fail(FO_ERR_SHAPE, "K must be a multiple of 64");
+    if (!fo::aligned16(A) || !fo::aligned16(W) || !fo::aligned16(C_out))
+        return fo::fail(FO_ERR_ARG, "A, W and C_out must be 16-byte aligned");
+    if (dev_plan && !fo::aligned16(dev_plan)) return fo::fail(FO_ERR_ARG, "dev_plan must be 16-byte aligned");
+    const fo_dev_layout& L = plan->layout;
+    fo::GemmArgs a{};
+    a.A = static_cast<const uint16_t*>(A);
+    a.W = static_cast<const uint16_t*>(W);
+    a.C = static_cast<uint16_t*>(C_out);
+    a.M = plan->M; a.N = plan->N; a.K = plan->K;
+    a.tiles_m = plan->tiles_m; a.tiles_n = plan->tiles_n;
+    a.order = plan->order; a.group_m = plan->group_m; a.num_xcds = plan->num_xcds;
+    a.pattern = plan->pattern; a.num_dest = plan->num_dest;
+    if (dev_plan) {
+        a.tile_to_slot = fo::dev_table<int32_t>(dev_plan, L.tile_to_slot);
+        a.slot_group = fo::dev_table<int32_t>(dev_plan, L.slot_group);
+        a.group_first = fo::dev_table<int32_t>(dev_plan, L.group_first);
+        a.row_bucket = fo::dev_table<int32_t>(dev_plan, L.row_bucket);
+        a.row_rank = fo::dev_table<int32_t>(dev_plan, L.row_rank);
+        a.pool_base = fo::dev_table<int32_t>(dev_plan, L.pool_base);
+        a.pool_off = fo::dev_table<int32_t>(dev_plan, L.pool_off);
+    }
+    a.counters = plan->P > 0 ? counters : nullptr;
+    hipError_t e = fo::launch_gemm(plan->dtype, plan->tile_m, plan->tile_n, a, plan->tiles,
+                                   (hipStream_t)stream);
+    return e == hipSuccess ? FO_OK : fo::hip_fail("GEMM launch", e);
+}
+
+fo_status fo_consume_group(const void* src, const void* peer, void* dst, int64_t len,
+                           int32_t dtype, const uint32_t* counter, uint32_t target,
+                           uint32_t* status_word, void* stream) {
+    fo::clear_error();
+    if (len < 0) return fo::fail(FO_ERR_ARG, "len < 0");
+    if (dtype != FO_FP16 && dtype != FO_BF16) return fo::fail(FO_ERR_ARG, "bad dtype");
+    if (len == 0 && !counter) return FO_OK;
+    if (len > 0 && (!src || !dst)) return fo::fail(FO_ERR_ARG, "null src or dst");
+    int64_t khz = 0;
+    fo_status st = fo::clock_khz(&khz);
+    if (st != FO_OK) return st;
+    const uint64_t ticks = (uint64_t)fo::poll_timeout_us() * (uint64_t)khz / 1000u;
+    hipError_t e = fo::launch_consume(dtype, static_cast<const uint16_t*>(src),
+                                      static_cast<const uint16_t*>(peer), static_cast<uint16_t*>(dst),
+                                      len, counter, target, status_word, ticks, (hipStream_t)stream);
+    return e == hipSuccess ? FO_OK : fo::hip_fail("consumer launch", e);
+}
+
+fo_status fo_post_reorder(const fo_plan* plan, const void* dev_plan, const void* src, void* out,
+                          const void* bias, const void* gamma, float eps, int32_t do_rmsnorm,
+                          void* stream) {
+    fo::clear_error();
+    if (!plan) return fo::fail(FO_ERR_ARG, "plan is NULL");
+    if (plan->M == 0 || plan->N == 0) return FO_OK;
+    if (!src || !out) return fo::fail(FO_ERR_ARG, "null src or out");
+    if (!dev_plan && plan->pattern != FO_PATTERN_ROWMAJOR) return fo::fail(FO_ERR_ARG, "dev_plan is NULL");
+    if (plan->N % 8 || plan->tile_n % 8) return fo::fail(FO_ERR_UNSUPPORTED, "N and tile_n must be multiples of 8");
+    if (!fo::aligned16(src) || !fo::aligned16(out) || (bias && !fo::aligned16(bias)) ||
+        (gamma && !fo::aligned16(gamma)))
+        return fo::fail(FO_ERR_ARG, "src, out, bias and gamma must be 16-byte aligned");
+    if (do_rmsnorm && !(eps >= 0.0f)) return fo::fail(FO_ERR_ARG, "eps must be >= 0");
+    const fo_dev_layout& L = plan->layout;
+    fo::PostArgs a{};
+    a.src = static_cast<const uint16_t*>(src);
+    a.out = static_cast<uint16_t*>(out);
+    a.bias = static_cast<const uint16_t*>(bias);
+    a.gamma = static_cast<const uint16_t*>(gamma);
+    a.M = plan->M; a.N = plan->N;
+    a.tile_m = plan->tile_m; a.tile_n = plan->tile_n; a.tiles_n = plan->tiles_n;
+    a.pattern = plan->pattern; a.num_dest = plan->num_dest;
+    a.per_dest = plan->pattern == FO_PATTERN_SUBTILE
+                     ? (int64_t)plan->tiles * (plan->tile_m / plan->num_dest) * plan->tile_n : 0;
+    if (dev_plan) {
+        a.tile_to_slot = fo::dev_table<int32_t>(dev_plan, L.tile_to_slot);
+        a.dest_perm = fo::dev_table<int32_t>(dev_plan, L.dest_perm);
+        a.row_bucket = fo::dev_table<int32_t>(dev_plan, L.row_bucket);
+        a.row_rank = fo::dev_table<int32_t>(dev_plan, L.row_rank);
+        a.pool_base = fo::dev_table<int32_t>(dev_plan, L.pool_base);
+        a.pool_off = fo::dev_table<int32_t>(dev_plan, L.pool_off);
+    }
+    a.eps = eps;
+    a.do_norm = do_rmsnorm ? 1 : 0;
+    hipError_t e = fo::launch_post(plan->dtype, a, (hipStream_t)stream);
+    return e == hipSuccess ? FO_OK : fo::hip_fail("post-reorder launch", e);
+}
+
+namespace {
+struct EventPair {
+    int device = -1;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+};
+thread_local EventPair t_events[8];
+
+fo_status events_for_current_device(hipEvent_t* e0, hipEvent_t* e1) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fo::hip_fail("hipGetDevice", e);
+    EventPair* slot = nullptr;
+    for (auto& p : t_events) {
+        if (p.device == dev) { slot = &p; break; }
+        if (!slot && p.device < 0) slot = &p;
+    }
+    if (!slot) return fo::fail(FO_ERR_UNSUPPORTED, "too many devices used from one thread");
+    if (slot->device != dev) {
+        if ((e = hipEventCreateWithFlags(&slot->e0, hipEventDisableTiming)) != hipSuccess)
+            return fo::hip_fail("hipEventCreate", e);
+        if ((e = hipEventCreateWithFlags(&slot->e1, hipEventDisableTiming)) != hipSuccess)
+            return fo::hip_fail("hipEventCreate", e);
+        slot->device = dev;
+    }
+    *e0 = slot->e0;
+    *e1 = slot->e1;
+    return FO_OK;
+}
+}  // namespace
+
+fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const void* A, const void* W,
+                            void* C_out, const void* peer, void* dst, void* out, const void* bias,
+                            const void* gamma, float eps, int32_t do_rmsnorm, uint32_t* counters,
+                            uint32_t* status_word, void* gemm_stream, void* comm_stream,
+                            void* gemm_begin_event, void* gemm_end_event) {
+    fo::clear_error();
+    if (!plan) return fo::fail(FO_ERR_ARG, "plan is NULL");
+    if (plan->tiles == 0) return FO_OK;
+    if (!dst) return fo::fail(FO_ERR_ARG, "dst is NULL");
+    const bool overlap = comm_stream && comm_stream != gemm_stream;
+    if (overlap && !counters) return fo::fail(FO_ERR_ARG, "an overlapped run needs counters");
+    hipStream_t s1 = (hipStream_t)gemm_stream, s2 = (hipStream_t)comm_stream;
+    fo_status st;
+    if (overlap) {
+        if ((st = fo_reset_counters(counters, plan->P, s1)) != FO_OK) return st;
+    }
+    if (status_word && (st = fo_reset_counters(status_word, 1, s1)) != FO_OK) return st;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    hipError_t e;
+    if (overlap) {
+        if ((st = events_for_current_device(&e0, &e1)) != FO_OK) return st;
+        if ((e = hipEventRecord(e0, s1)) != hipSuccess) return fo::hip_fail("hipEventRecord", e);
+        if ((e = hipStreamWaitEvent(s2, e0, 0)) != hipSuccess) return fo::hip_fail("hipStreamWaitEvent", e);
+    }
+    if (gemm_begin_event && (e = hipEventRecord((hipEvent_t)gemm_begin_event, s1)) != hipSuccess)
+        return fo::hip_fail("hipEventRecord", e);
+    if ((st = fo_gemm_signal_reorder(plan, dev_plan, A, W, C_out, overlap ? counters : nullptr, s1)) != FO_OK)
+        return st;
+    if (gemm_end_event && (e = hipEventRecord((hipEvent_t)gemm_end_event, s1)) != hipSuccess)
+        return fo::hip_fail("hipEventRecord", e);
+    const int64_t* seg = plan->segs.data();
+    const int nseg = (int)(plan->segs.size() / 5);
+    const uint16_t* src16 = static_cast<const uint16_t*>(C_out);
+    const uint16_t* peer16 = static_cast<const uint16_t*>(peer);
+    uint16_t* dst16 = static_cast<uint16_t*>(dst);
+    for (int i = 0; i < nseg; ++i) {
+        const int64_t j = seg[5 * i], so = seg[5 * i + 2], dof = seg[5 * i + 3], len = seg[5 * i + 4];
+        if (len == 0) continue;
+        st = fo_consume_group(src16 + so, peer16 ? peer16 + so : nullptr, dst16 + dof, len, plan->dtype,
+                              overlap ? counters + j : nullptr, (uint32_t)plan->targets[j], status_word,
+                              overlap ? s2 : s1);
+        if (st != FO_OK) return st;
+    }
+    if (overlap) {
+        if ((e = hipEventRecord(e1, s2)) != hipSuccess) return fo::hip_fail("hipEventRecord", e);
+        if ((e = hipStreamWaitEvent(s1, e1, 0)) != hipSuccess) return fo::hip_fail("hipStreamWaitEvent", e);
+    }
+    if (out) return fo_post_reorder(plan, dev_plan, dst, out, bias, gamma, eps, do_rmsnorm, s1);
+    return FO_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,209 @@
+"""GPU parity of each kernel against the oracle, through the C ABI.
+
+GEMM values: within |err| <= 2e-3 + 1e-2 |ref| of the exact product rounded
+once. Everything that only moves or rounds sums of two stored values is
+bit-exact: the reordered output against the oracle's permutation of the GPU's
+own plain GEMM output, the counters against the group tile counts, the
+consumer sum, the post-reorder gather and the bias add.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2504_19519_amd as fo
+import workloads
+from gpu_util import (assert_close_bits, dev_plan, empty16, from_dev, say, to_dev, zeros_u32,
+                      torch_mod)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    torch = torch_mod()
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    fo.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _operands(M, N, K, dtype, seed):
+    rng = np.random.default_rng(seed)
+    A = workloads.to_bits(rng.uniform(-1, 1, (M, K)), dtype)
+    W = workloads.to_bits(rng.uniform(-1, 1, (N, K)) / np.sqrt(max(K, 1)), dtype)
+    return A, W
+
+
+def _gemm(plan, A, W, counters=None, poison=None):
+    torch = torch_mod()
+    dA, dW = to_dev(A), to_dev(W)
+    C = empty16(plan.M * plan.N, poison)
+    dp = dev_plan(plan)
+    fo.gemm_signal_reorder(plan, dp, dA, dW, C, counters)
+    torch.cuda.synchronize()
+    return from_dev(C)[:plan.M * plan.N]
+
+
+@pytest.mark.parametrize("dtype", ["fp16", "bf16"])
+@pytest.mark.parametrize("tile,shape", [((256, 128), (512, 384, 320)),
+                                        ((256, 128), (1024, 640, 192)),
+                                        ((64, 64), (256, 256, 256)),
+                                        ((64, 64), (192, 320, 128))])
+def test_plain_gemm_matches_oracle(dtype, tile, shape):
+    M, N, K = shape
+    say(f"[gemm rowmajor] dtype={dtype} tile={tile} M={M} N={N} K={K}")
+    A, W = _operands(M, N, K, dtype, 11)
+    plan = fo.plan_groups(M, N, K, dtype=dtype, tile_m=tile[0], tile_n=tile[1], order="xcd",
+                          num_cus=4, pattern="rowmajor", sizes=None, curve_bytes=[1.0], curve_us=[0.0])
+    C = _gemm(plan, A, W, poison=dtype)
+    assert_close_bits(C, oracle.gemm_ref(A, W, dtype).reshape(-1), dtype, "plain GEMM")
+
+
+@pytest.mark.parametrize("dtype", ["fp16", "bf16"])
+@pytest.mark.parametrize("tile", [(256, 128), (64, 64)])
+def test_identity_operand_is_exact(dtype, tile):
+    # A = I: every output is one product by 1 plus sums of zeros, so C = B
+    # exactly, whatever the accumulation order (pins the epilogue layout).
+    K = N = M = 256
+    say(f"[gemm identity] dtype={dtype} tile={tile}")
+    A = workloads.to_bits(np.eye(K), dtype)
+    _, W = _operands(M, N, K, dtype, 12)
+    plan = fo.plan_groups(M, N, K, dtype=dtype, tile_m=tile[0], tile_n=tile[1], num_cus=4,
+                          pattern="rowmajor", sizes=[-(-((M // tile[0]) * (N // tile[1])) // 4)])
+    C = _gemm(plan, A, W, poison=dtype).reshape(M, N)
+    np.testing.assert_array_equal(C, W.T)
+
+
+def test_k_zero_gives_zeros():
+    M, N = 256, 128
+    say("[gemm K=0]")
+    plan = fo.plan_groups(M, N, 0, pattern="rowmajor", num_cus=4, sizes=[1])
+    A = np.zeros(8, np.uint16)
+    C = _gemm(plan, A, A, poison="fp16")
+    assert np.all(C == 0)
+
+
+@pytest.mark.parametrize("pattern,nd", [("tile", 0), ("subtile", 4), ("subtoken", 8), ("rowmajor", 0)])
+@pytest.mark.parametrize("dtype", ["fp16", "bf16"])
+@pytest.mark.parametrize("sizes", [(1, 2), (3,), (1, 1, 1)])
+def test_reordered_output_is_permuted_plain_output(pattern, nd, dtype, sizes):
+    # 4 x 5 tiles of 256x128 on a modelled 8-CU device: W = 8, T = 3 with a
+    # 4-tile last wave; the XCD order with 8 chiplets on 20 tiles is ragged.
+    M, N, K = 1024, 640, 256
+    say(f"[reorder] pattern={pattern} dtype={dtype} sizes={sizes}")
+    rng = np.random.default_rng(13)
+    A, W = _operands(M, N, K, dtype, 14)
+    sigma = rng.permutation(nd) if pattern == "subtile" else None
+    bucket = rng.integers(0, nd, M) if pattern == "subtoken" else None
+    common = dict(dtype=dtype, order="xcd", num_cus=8, num_dest=nd, dest_perm=sigma, row_bucket=bucket)
+    plain = fo.plan_groups(M, N, K, pattern="rowmajor", sizes=list(sizes), **common)
+    C = _gemm(plain, A, W, poison=dtype)
+    plan = fo.plan_groups(M, N, K, pattern=pattern, sizes=list(sizes), **common)
+    o = oracle.make_plan(M, N, 256, 128, num_cus=8, order="xcd", pattern=pattern, num_dest=nd,
+                         sigma=sigma, bucket=bucket, sizes=sizes)
+    counters = zeros_u32(plan.P)
+    Cr = _gemm(plan, A, W, counters=counters, poison=dtype)
+    np.testing.assert_array_equal(Cr, C[oracle.reorder_index(o)])
+    np.testing.assert_array_equal(counters.cpu().numpy()[:plan.P], np.array(o.targets))
+
+
+@pytest.mark.parametrize("dtype", ["fp16", "bf16"])
+@pytest.mark.parametrize("length", [1, 7, 8, 4096 + 3, 1_000_003, 8 * 1024 * 1024 + 5])
+@pytest.mark.parametrize("offset", [0, 1])
+@pytest.mark.parametrize("mode", ["sum", "copy"])
+def test_consumer_bit_exact(dtype, length, offset, mode):
+    torch = torch_mod()
+    say(f"[consume] dtype={dtype} len={length} offset={offset} mode={mode}")
+    src = workloads.uniform_bits(length + 8, 21, dtype, -4, 4)
+    peer = workloads.uniform_bits(length + 8, 22, dtype, -4, 4)
+    dS, dP = to_dev(src), to_dev(peer)
+    dD = empty16(length + 8, dtype)
+    ctr = zeros_u32(1)
+    ctr.fill_(5)
+    el = 2
+    fo.consume_group(dS.data_ptr() + el * offset, dP.data_ptr() + el * offset if mode == "sum" else None,
+                     dD.data_ptr() + el * offset, length, dtype, ctr, 5)
+    torch.cuda.synchronize()
+    got = from_dev(dD)[offset:offset + length]
+    s, p = src[offset:offset + length], peer[offset:offset + length]
+    ref = oracle.add_rne(s, p, dtype) if mode == "sum" else s
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_consumer_timeout_reports_and_skips():
+    torch = torch_mod()
+    say("[consume timeout] counter never reaches the target; 2 ms limit")
+    old = fo.get_poll_timeout_us()
+    fo.set_poll_timeout_us(2000)
+    try:
+        n = 4096
+        src = workloads.uniform_bits(n, 23)
+        dS = to_dev(src)
+        dD = empty16(n, "fp16")
+        ctr = zeros_u32(1)
+        status = zeros_u32(1)
+        fo.consume_group(dS, None, dD, n, "fp16", ctr, 1, status)
+        torch.cuda.synchronize()
+        assert int(status.cpu()[0]) & 1
+        assert np.all(from_dev(dD)[:n] == 0x7E00)
+    finally:
+        fo.set_poll_timeout_us(old)
+
+
+def _post_case(pattern, nd, M, N, BM, BN, dtype, seed):
+    rng = np.random.default_rng(seed)
+    sigma = rng.permutation(nd) if pattern == "subtile" else None
+    bucket = rng.integers(0, nd, M) if pattern == "subtoken" else None
+    tiles = (M // BM) * (N // BN)
+    plan = fo.plan_groups(M, N, 64, dtype=dtype, tile_m=BM, tile_n=BN, order="xcd", num_cus=16,
+                          pattern=pattern, num_dest=nd, dest_perm=sigma, row_bucket=bucket,
+                          sizes=[-(-tiles // 16)])
+    o = oracle.make_plan(M, N, BM, BN, num_cus=16, order="xcd", pattern=pattern, num_dest=nd,
+                         sigma=sigma, bucket=bucket, sizes=(-(-tiles // 16),))
+    return plan, o
+
+
+@pytest.mark.parametrize("pattern,nd", [("tile", 0), ("subtile", 4), ("subtoken", 8), ("rowmajor", 0)])
+@pytest.mark.parametrize("N", [256, 4096, 7168, 16384])
+@pytest.mark.parametrize("dtype", ["fp16", "bf16"])
+def test_post_reorder(pattern, nd, N, dtype):
+    torch = torch_mod()
+    M, BM, BN = 512, 256, 128
+    say(f"[post] pattern={pattern} N={N} dtype={dtype}")
+    plan, o = _post_case(pattern, nd, M, N, BM, BN, dtype, 31)
+    dst = workloads.uniform_bits(plan.dest_elems, 32, dtype, -3, 3)
+    bias = workloads.uniform_bits(N, 33, dtype, -0.1, 0.1)
+    gamma = workloads.uniform_bits(N, 34, dtype, 0.5, 1.5)
+    dD, dB, dG = to_dev(dst), to_dev(bias), to_dev(gamma)
+    dp = dev_plan(plan)
+    x_ref = dst[oracle.post_index(o)].reshape(M, N)
+    out = empty16(M * N, dtype)
+    fo.post_reorder(plan, dp, dD, out)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(from_dev(out)[:M * N].reshape(M, N), x_ref)
+    fo.post_reorder(plan, dp, dD, out, bias=dB)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(from_dev(out)[:M * N].reshape(M, N),
+                                  oracle.rmsnorm(x_ref, dtype, bias=bias, do_norm=False))
+    fo.post_reorder(plan, dp, dD, out, bias=dB, gamma=dG, eps=1e-6, do_rmsnorm=True)
+    torch.cuda.synchronize()
+    assert_close_bits(from_dev(out)[:M * N], oracle.rmsnorm(x_ref, dtype, bias=bias, gamma=gamma, eps=1e-6),
+                      dtype, "post + bias + RMSNorm")
+    fo.post_reorder(plan, dp, dD, out, eps=1e-6, do_rmsnorm=True)
+    torch.cuda.synchronize()
+    assert_close_bits(from_dev(out)[:M * N], oracle.rmsnorm(x_ref, dtype, eps=1e-6), dtype, "post + RMSNorm")
+
+
+def test_bad_arguments_are_rejected_before_launch():
+    plan = fo.plan_groups(512, 256, 100, num_cus=4, pattern="rowmajor", sizes=[1])
+    with pytest.raises(fo.FoError) as e:
+        fo.gemm_signal_reorder(plan, None, 256, 256, 256)
+    assert e.value.status == -2           # K % 64
+    plan = fo.plan_groups(512, 256, 64, num_cus=4, pattern="tile", sizes=[1])
+    with pytest.raises(fo.FoError):
+        fo.gemm_signal_reorder(plan, None, 256, 256, 256)     # tile pattern needs dev_plan
+    with pytest.raises(fo.FoError):
+        fo.consume_group(0, None, 0, 10, "fp16")
+    with pytest.raises(fo.FoError):
+        fo.consume_group(256, None, 256, -1, "fp16")

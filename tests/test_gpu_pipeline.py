@@ -1,0 +1,174 @@
+"""The whole path on the GPU (plan -> signalling GEMM on one stream ||
+consumers on a second stream -> post-reorder), against the oracle.
+
+For every workload: the reordered GEMM output is the oracle's permutation of
+the GPU's plain GEMM output (bit-exact), the consumer output is the oracle's
+consumer applied to it (bit-exact), the restored output is the oracle's
+post-reorder of that (bit-exact, or within the fp16/bf16 tolerance when
+RMSNorm runs), every counter ends at its group's tile count, and the GEMM
+values match the exact product (all outputs at small sizes, a seeded sample of
+rows at the full sizes). Destination buffers are filled with NaN before each
+run, so a consumer that read a group early would leave NaNs behind.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2504_19519_amd as fo
+import workloads
+from gpu_util import (assert_close_bits, dev_plan, empty16, from_dev, plan_for, say, to_dev,
+                      torch_mod, zeros_u32)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    torch = torch_mod()
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    fo.lib()
+
+
+class Dev:
+    """Device copies of one workload's inputs."""
+
+    def __init__(self, w, inp, plan):
+        self.A, self.W = to_dev(inp.A), to_dev(inp.W)
+        self.peer = to_dev(inp.peer) if w.pattern != "subtoken" else None
+        self.bias = to_dev(inp.bias) if inp.bias is not None else None
+        self.gamma = to_dev(inp.gamma) if inp.gamma is not None else None
+        self.dp = dev_plan(plan)
+
+
+def run(w, plan, d: Dev, *, overlap=True):
+    torch = torch_mod()
+    C = empty16(w.M * w.N, w.dtype)
+    dst = empty16(plan.dest_elems, w.dtype)
+    out = empty16(w.M * w.N, w.dtype)
+    counters = zeros_u32(plan.P)
+    status = zeros_u32(1)
+    s1 = torch.cuda.Stream()
+    s2 = torch.cuda.Stream() if overlap else s1
+    torch.cuda.synchronize()
+    fo.run_overlapped(plan, d.dp, d.A, d.W, C, d.peer, dst, out, d.bias, d.gamma, w.eps,
+                      w.rmsnorm, counters, status, s1, s2)
+    torch.cuda.synchronize()
+    n = w.M * w.N
+    return (from_dev(C)[:n], from_dev(dst)[:plan.dest_elems], from_dev(out)[:n],
+            counters.cpu().numpy()[:plan.P], int(status.cpu()[0]))
+
+
+def plain_gemm(w, d: Dev, plan_rm):
+    torch = torch_mod()
+    C = empty16(w.M * w.N, w.dtype)
+    fo.gemm_signal_reorder(plan_rm, None, d.A, d.W, C, None)
+    torch.cuda.synchronize()
+    return from_dev(C)[:w.M * w.N]
+
+
+def check(w, inp, plan, o, sample_rows=None):
+    d = Dev(w, inp, plan)
+    plan_rm = fo.plan_groups(w.M, w.N, w.K, dtype=w.dtype, tile_m=w.tile_m, tile_n=w.tile_n,
+                             order=w.order, num_cus=256, pattern="rowmajor",
+                             sizes=None, curve_bytes=[1.0], curve_us=[0.0])
+    C_plain = plain_gemm(w, d, plan_rm)
+    # GEMM values against the exact product
+    if sample_rows is None:
+        assert_close_bits(C_plain, oracle.gemm_ref(inp.A, inp.W, w.dtype).reshape(-1), w.dtype, "GEMM")
+    else:
+        rows = np.sort(np.random.default_rng(w.seed + 1000).choice(w.M, sample_rows, replace=False))
+        ref = oracle.encode(oracle.gemm_exact(inp.A, inp.W, w.dtype, rows=rows), w.dtype)
+        assert_close_bits(C_plain.reshape(w.M, w.N)[rows], ref, w.dtype, "GEMM (sampled rows)")
+    Cr, dst, out, counters, status = run(w, plan, d, overlap=True)
+    assert status == 0
+    np.testing.assert_array_equal(counters, np.array(o.targets))
+    np.testing.assert_array_equal(Cr, C_plain[oracle.reorder_index(o)])
+    dst_ref = oracle.apply_consumer(o, Cr, inp.peer if w.pattern != "subtoken" else None, w.dtype)
+    np.testing.assert_array_equal(dst, dst_ref)
+    x = dst_ref[oracle.post_index(o)].reshape(w.M, w.N)
+    if w.rmsnorm:
+        ref = oracle.rmsnorm(x, w.dtype, bias=inp.bias, gamma=inp.gamma, eps=w.eps)
+        assert_close_bits(out, ref, w.dtype, "post + RMSNorm")
+    elif inp.bias is not None:
+        np.testing.assert_array_equal(out.reshape(w.M, w.N), oracle.rmsnorm(x, w.dtype, bias=inp.bias, do_norm=False))
+    else:
+        np.testing.assert_array_equal(out.reshape(w.M, w.N), x)
+    # the same work serialized on one stream gives the same bits
+    Cr2, dst2, out2, counters2, status2 = run(w, plan, d, overlap=False)
+    assert status2 == 0
+    np.testing.assert_array_equal(Cr2, Cr)
+    np.testing.assert_array_equal(dst2, dst)
+    np.testing.assert_array_equal(out2, out)
+    return C_plain, out
+
+
+SMALL = {
+    # workload: (M, N, K, modelled CUs, partition in waves)
+    "tiny": None,
+    "ar_2048x4096x4096": (1024, 1024, 512, 8, (1, 2, 1)),
+    "rs_8192x8192x3584": (1024, 1024, 512, 8, (2, 1, 1)),
+    "ar_rmsnorm_16384x4096x3584_bf16": (1024, 1024, 512, 8, (1, 1, 2)),
+    "a2a_4096x7168x2048": (1024, 896, 512, 8, (1, 1, 2)),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_small_workloads(name):
+    w = workloads.WORKLOADS[name]
+    cus, sizes = 256, None
+    if SMALL[name] is not None:
+        M, N, K, cus, sizes = SMALL[name]
+        w = w.with_shape(M, N, K)
+    say(f"[pipeline small] {w.name} cus={cus} sizes={sizes}")
+    inp = workloads.make_inputs(w)
+    plan, o = plan_for(w, inp, num_cus=cus, sizes=list(sizes) if sizes else None)
+    C_plain, out = check(w, inp, plan, o)
+    # end to end against the oracle's own chain from the exact GEMM
+    C_ref = oracle.gemm_ref(inp.A, inp.W, w.dtype)
+    _, _, out_ref = oracle.run_path(o, C_ref, inp.peer if w.pattern != "subtoken" else None, w.dtype,
+                                    bias=inp.bias, gamma=inp.gamma, eps=w.eps, do_norm=w.rmsnorm)
+    assert_close_bits(out, out_ref, w.dtype, "end to end")
+
+
+FULL = {
+    "ar_2048x4096x4096": [(1,)],
+    "rs_8192x8192x3584": [(1,) * 8, (2, 2, 2, 2)],
+    "ar_rmsnorm_16384x4096x3584_bf16": [(1,) * 8],
+    "a2a_4096x7168x2048": [(1, 1, 1, 1)],
+}
+
+
+@pytest.mark.parametrize("name,sizes", [(n, s) for n, ss in FULL.items() for s in ss])
+def test_full_size_workloads(name, sizes):
+    w = workloads.WORKLOADS[name]
+    say(f"[pipeline full] {w.name} sizes={sizes}")
+    inp = workloads.make_inputs(w)
+    plan, o = plan_for(w, inp, num_cus=256, sizes=list(sizes))
+    check(w, inp, plan, o, sample_rows=24)
+
+
+def test_consumers_wait_for_a_delayed_gemm():
+    # the consumers are enqueued and start polling before the GEMM is even
+    # launched (the GEMM stream first runs a ~20 ms spin kernel)
+    torch = torch_mod()
+    w = workloads.WORKLOADS["ar_2048x4096x4096"].with_shape(1024, 1024, 512)
+    say("[pipeline delayed GEMM]")
+    inp = workloads.make_inputs(w)
+    plan, o = plan_for(w, inp, num_cus=8, sizes=[1, 1, 1, 1])
+    d = Dev(w, inp, plan)
+    C = empty16(w.M * w.N, w.dtype)
+    dst = empty16(plan.dest_elems, w.dtype)
+    counters = zeros_u32(plan.P)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for (j, _, so, do, ln) in plan.segments:
+        fo.consume_group(C.data_ptr() + 2 * so, d.peer.data_ptr() + 2 * so, dst.data_ptr() + 2 * do,
+                         ln, w.dtype, counters.data_ptr() + 4 * j, int(plan.targets[j]), None, s2)
+    with torch.cuda.stream(s1):
+        torch.cuda._sleep(50_000_000)
+    fo.gemm_signal_reorder(plan, d.dp, d.A, d.W, C, counters, s1)
+    torch.cuda.synchronize()
+    Cr = from_dev(C)[:w.M * w.N]
+    ref = oracle.apply_consumer(o, Cr, inp.peer, w.dtype)
+    np.testing.assert_array_equal(from_dev(dst)[:plan.dest_elems], ref)

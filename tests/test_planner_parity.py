@@ -1,0 +1,163 @@
+"""Host planner (libfo's fo_plan_groups) against the oracle's plan, bit for
+bit: dispatch order, reorder map, groups, counter targets, segments, pools,
+and the Algorithm 1 choice. Runs on the CPU (no GPU call is made)."""
+import math
+import re
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2504_19519_amd as fo
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _both(M, N, BM, BN, *, cus, order="xcd", group_m=4, num_xcds=8, pattern="tile", nd=0,
+          sigma=None, bucket=None, sizes=None, unit="waves", wg_per_cu=1, reserved=0):
+    p = fo.plan_groups(M, N, 64, tile_m=BM, tile_n=BN, order=order, group_m=group_m,
+                       num_xcds=num_xcds, num_cus=cus, wg_per_cu=wg_per_cu, reserved_cus=reserved,
+                       pattern=pattern, num_dest=nd, dest_perm=sigma, row_bucket=bucket,
+                       sizes=sizes, unit=unit)
+    o = oracle.make_plan(M, N, BM, BN, num_cus=cus, wg_per_cu=wg_per_cu, reserved_cus=reserved,
+                         order=order, group_m=group_m, num_xcds=num_xcds, pattern=pattern,
+                         num_dest=nd, sigma=sigma, bucket=bucket, sizes=sizes, unit=unit)
+    return p, o
+
+
+def _compare(p, o):
+    assert p.tiles == o.tiles and p.W == o.W and p.T == o.T and p.P == o.P
+    np.testing.assert_array_equal(p.order, np.array(o.order))
+    np.testing.assert_array_equal(p.tile_to_slot, o.tile_to_slot)
+    np.testing.assert_array_equal(p.group_first, np.array(o.first))
+    np.testing.assert_array_equal(p.targets, np.array(o.targets))
+    np.testing.assert_array_equal(p.segments, np.array(oracle.segments(o), dtype=np.int64).reshape(-1, 5))
+    assert p.dest_elems == oracle.dest_buffer_elems(o)
+    if o.pattern == "subtoken":
+        np.testing.assert_array_equal(p.pool_base, o.pool_base)
+        np.testing.assert_array_equal(p.pool_off, o.pool_off)
+
+
+def _workload_plan_args(w: workloads.Workload, inp=None):
+    kw = dict(cus=256, order=w.order, pattern=w.pattern, nd=w.num_dest if w.pattern in ("subtile", "subtoken") else 0)
+    if w.pattern == "subtile":
+        kw["sigma"] = np.random.default_rng(w.seed).permutation(w.num_dest)
+    if w.pattern == "subtoken":
+        kw["bucket"] = np.random.default_rng(w.seed).integers(0, w.num_dest, w.M)
+    return kw
+
+
+@pytest.mark.parametrize("name", list(workloads.WORKLOADS))
+def test_workload_plans_match_oracle(name):
+    w = workloads.WORKLOADS[name]
+    kw = _workload_plan_args(w)
+    tiles = (w.M // w.tile_m) * (w.N // w.tile_n)
+    T = -(-tiles // 256)
+    if w.groups is not None:
+        sizes, unit = list(w.groups), w.group_unit
+    else:
+        sizes, unit = [1] * T, "waves"
+    p, o = _both(w.M, w.N, w.tile_m, w.tile_n, sizes=sizes, unit=unit, **kw)
+    _compare(p, o)
+
+
+@pytest.mark.parametrize("pattern,nd", [("tile", 0), ("subtile", 4), ("subtoken", 8), ("rowmajor", 0)])
+@pytest.mark.parametrize("order", ["rowmajor", "grouped", "xcd"])
+@pytest.mark.parametrize("shape", [(1024, 640, 256, 128, 8, (1, 2)),     # 20 tiles, W=8, T=3
+                                   (768, 384, 64, 64, 5, (2, 1, 3, 1)),   # 72 tiles, W=5, T=15 -> sizes sum 7? fixed below
+                                   (512, 1024, 256, 128, 3, None)])
+def test_small_plans_match_oracle(pattern, nd, order, shape):
+    M, N, BM, BN, cus, sizes = shape
+    rng = np.random.default_rng(7)
+    tiles = (M // BM) * (N // BN)
+    T = -(-tiles // cus)
+    if sizes is None or sum(sizes) != T:
+        # a deterministic irregular partition of T waves
+        sizes, left = [], T
+        while left:
+            s = min(left, int(rng.integers(1, 4)))
+            sizes.append(s)
+            left -= s
+    kw = dict(cus=cus, order=order, group_m=3, num_xcds=8 if order == "xcd" else 1,
+              pattern=pattern, nd=nd, sizes=sizes)
+    if pattern == "subtile":
+        kw["sigma"] = rng.permutation(nd)
+    if pattern == "subtoken":
+        kw["bucket"] = rng.integers(0, nd, M)
+    p, o = _both(M, N, BM, BN, **kw)
+    _compare(p, o)
+
+
+def test_tile_unit_and_reserved_cus():
+    p, o = _both(2048, 1024, 256, 128, cus=16, reserved=3, wg_per_cu=2, sizes=[5, 20, 39], unit="tiles")
+    _compare(p, o)
+    assert p.W == (16 - 3) * 2
+
+
+def _curve(seed):
+    rng = np.random.default_rng(seed)
+    xs = np.sort(rng.uniform(1e4, 5e8, 12))
+    bw = rng.uniform(0.5e3, 6e3, 12)            # bytes per us
+    ys = np.maximum.accumulate(xs / bw + rng.uniform(2, 10))
+    return xs, ys
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("pattern,nd", [("tile", 0), ("subtoken", 8), ("subtile", 4)])
+def test_predictive_search_matches_oracle(seed, pattern, nd):
+    rng = np.random.default_rng(100 + seed)
+    M, N, BM, BN = 4096, 7168, 256, 128      # 896 tiles, 3.5 waves at 256 CUs
+    cus = int(rng.choice([64, 128, 256]))
+    xs, ys = _curve(seed)
+    gemm_us = float(rng.uniform(20, 400))
+    bucket = rng.integers(0, nd, M) if pattern == "subtoken" else None
+    sigma = rng.permutation(nd) if pattern == "subtile" else None
+    p = fo.plan_groups(M, N, 2048, num_cus=cus, pattern=pattern, num_dest=nd, row_bucket=bucket,
+                       dest_perm=sigma, sizes=None, gemm_us=gemm_us, curve_bytes=xs, curve_us=ys,
+                       s_first=2, s_last=4)
+    o = oracle.make_plan(M, N, BM, BN, num_cus=cus, order="xcd", pattern=pattern, num_dest=nd,
+                         bucket=bucket, sigma=sigma, sizes=(-(-896 // cus),))
+    best, t = oracle.search_partition(o, gemm_us, xs, ys, 2, 4)
+    assert tuple(p.sizes) == best
+    assert p.predicted_us == pytest.approx(t, rel=1e-12)
+
+
+def test_search_single_wave_gives_one_group():
+    # 2048 x 4096 in 256x128 tiles is 256 tiles: one wave on 256 CUs
+    p = fo.plan_groups(2048, 4096, 4096, num_cus=256, sizes=None, gemm_us=40.0,
+                       curve_bytes=[1e6, 1e8], curve_us=[5.0, 20.0])
+    assert p.T == 1 and list(p.sizes) == [1] and list(p.targets) == [256]
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(M=1000, N=1024, K=64), -2),                          # M % tile_m
+    (dict(M=1024, N=1024, K=64, sizes=[1, 1, 1]), -1),         # sizes do not sum to T
+    (dict(M=1024, N=1024, K=64, pattern="subtile", num_dest=3, sizes=[1]), -2),   # 256 % 3
+    (dict(M=1024, N=1024, K=64, pattern="subtoken", num_dest=4, sizes=[1]), -1),  # no row_bucket
+    (dict(M=1024, N=1024, K=64, pattern="subtile", num_dest=4, dest_perm=[0, 0, 1, 2], sizes=[1]), -1),
+    (dict(M=1024, N=1024, K=64, sizes=None), -1),              # search without a curve
+    (dict(M=1024, N=1024, K=64, num_cus=0, sizes=[1]), -1),
+    (dict(M=256 * 64, N=128 * 64, K=64, num_cus=16, sizes=None, curve_bytes=[1.0], curve_us=[1.0]), -3),
+])
+def test_plan_errors(kwargs, status):
+    with pytest.raises(fo.FoError) as e:
+        fo.plan_groups(**kwargs)
+    assert e.value.status == status
+
+
+def test_empty_problem():
+    p = fo.plan_groups(0, 1024, 64, sizes=None, curve_bytes=[1.0], curve_us=[1.0])
+    assert p.tiles == 0 and p.T == 0 and p.P == 0 and p.segments.shape == (0, 5)
+
+
+def test_header_symbols_are_exported():
+    with open(os.path.join(ROOT, "include", "fo.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = set(re.findall(r"\b(fo_[a-z0-9_]+)\s*\(", text))
+    assert len(names) >= 25
+    L = fo.lib()
+    missing = [n for n in sorted(names) if not hasattr(L, n)]
+    assert not missing, missing
