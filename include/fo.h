@@ -284,6 +284,28 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan,
                             uint32_t* status_word, void* gemm_stream, void* comm_stream,
                             void* gemm_begin_event, void* gemm_end_event);
 
+/*
+ * How the producer (GEMM epilogue) publishes a finished tile and how the
+ * consumer reads a signalled group. All modes are correct; they differ in
+ * the cache maintenance they cost (MI355X has one L2 per chiplet):
+ *   FO_SYNC_FENCE_ALL: producer: every wave makes its stores visible with an
+ *     agent-scope release fence (L2 write-back), then one lane increments;
+ *     consumer: every wave invalidates its caches with an agent-scope acquire.
+ *   FO_SYNC_FENCE_ONE: producer: workgroup barrier, then one agent-scope
+ *     release increment; consumer: one acquire (wave 0) before a workgroup
+ *     barrier.
+ *   FO_SYNC_COHERENT: producer: the tile is written with device-coherent
+ *     stores that go through to the memory side shared by all chiplets, every
+ *     wave waits for their completion, then one lane increments (no
+ *     write-back); consumer: the group is read with device-coherent loads
+ *     after the counter is seen (no invalidation).
+ * Default: FO_SYNC_COHERENT for both; env FO_SYNC_PRODUCER / FO_SYNC_CONSUMER
+ * (0, 1, 2) override at load time. Process-wide.
+ */
+typedef enum { FO_SYNC_FENCE_ALL = 0, FO_SYNC_FENCE_ONE = 1, FO_SYNC_COHERENT = 2 } fo_sync_mode;
+fo_status fo_set_sync_mode(int32_t producer, int32_t consumer);
+void fo_get_sync_mode(int32_t* producer, int32_t* consumer);
+
 /* Upper bound of one consumer wait, in microseconds (default 2 s; env
  * FO_POLL_TIMEOUT_US overrides at load time). */
 void fo_set_poll_timeout_us(int64_t us);

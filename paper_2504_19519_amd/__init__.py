@@ -20,7 +20,7 @@ import numpy as np
 __all__ = [
     "FoError", "Plan", "plan_groups", "gemm_signal_reorder", "consume_group",
     "post_reorder", "reset_counters", "run_overlapped", "set_poll_timeout_us",
-    "get_poll_timeout_us", "device_num_cus", "LIB_PATH",
+    "get_poll_timeout_us", "device_num_cus", "set_sync_mode", "get_sync_mode", "LIB_PATH",
     "FP16", "BF16", "TILE", "SUBTILE", "SUBTOKEN", "ROWMAJOR",
 ]
 
@@ -99,6 +99,8 @@ def lib() -> ctypes.CDLL:
     L.fo_reset_counters.argtypes = [vp, i32, vp]
     L.fo_run_overlapped.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, i32,
                                     vp, vp, vp, vp, vp, vp]
+    L.fo_set_sync_mode.argtypes, L.fo_set_sync_mode.restype = [i32, i32], ctypes.c_int
+    L.fo_get_sync_mode.argtypes = [pi32, pi32]
     L.fo_set_poll_timeout_us.argtypes = [i64]
     L.fo_get_poll_timeout_us.restype = i64
     L.fo_device_num_cus.argtypes = [i32, pi32]
@@ -299,6 +301,19 @@ def run_overlapped(plan: Plan, dev_plan, A, W, C_out, peer, dst, out=None, bias=
                                    float(eps), int(bool(do_rmsnorm)), _ptr(counters),
                                    _ptr(status_word), _stream(gemm_stream), _stream(comm_stream),
                                    _event(gemm_begin_event), _event(gemm_end_event)))
+
+
+SYNC_FENCE_ALL, SYNC_FENCE_ONE, SYNC_COHERENT = 0, 1, 2
+
+
+def set_sync_mode(producer: int, consumer: int) -> None:
+    _check(lib().fo_set_sync_mode(int(producer), int(consumer)))
+
+
+def get_sync_mode():
+    p, c = ctypes.c_int32(), ctypes.c_int32()
+    lib().fo_get_sync_mode(ctypes.byref(p), ctypes.byref(c))
+    return int(p.value), int(c.value)
 
 
 def set_poll_timeout_us(us: int) -> None:

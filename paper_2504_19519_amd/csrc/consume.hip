@@ -4,15 +4,16 @@
 // is a library call on a contiguous buffer, Section 3.3 Motivation).
 //
 // One launch handles one contiguous segment: every workgroup waits for the
-// group's counter (relaxed agent-scope polls with s_sleep, then one
-// agent-scope acquire), then streams the segment:
+// group's counter (relaxed agent-scope polls with s_sleep; then an
+// agent-scope acquire, or device-coherent loads of the segment, see
+// fo_sync_mode), then streams the segment:
 //   dst = RNE(src + peer)   AllReduce / ReduceScatter of two partials
 //   dst = src               All-to-All (copy to the receive buffer)
 // The wait is bounded by a wall-clock limit; on timeout the workgroup writes
 // nothing and raises bit 0 of the status word, so a missing signal can never
 // hang the device.
 //
-// The grid is capped (kMaxBlocks) and a workgroup holds no LDS and few
+// The grid is capped (kMaxConsumeBlocks) and a workgroup holds no LDS and few
 // registers, so polling workgroups never take the resources a not yet
 // dispatched GEMM workgroup needs (the GEMM holds 110 KB of LDS, four waves
 // and about half of each SIMD's registers per CU).
@@ -28,6 +29,13 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kUnroll = 4;
 
+// Wait until *counter >= target. Thread 0 polls with relaxed agent-scope
+// loads (device-coherent, no cache invalidation) and sleeps between polls.
+// SYNC == FENCE_ALL: thread 0 and then every wave take an agent-scope
+// acquire (cache invalidation); FENCE_ONE: thread 0 only (its invalidation
+// covers the CU's L1 and the chiplet's L2 that the whole workgroup uses);
+// COHERENT: no acquire, the data is then read with device-coherent loads.
+template <int SYNC>
 __device__ __forceinline__ bool wait_counter(const uint32_t* counter, uint32_t target,
                                              uint32_t* status, uint64_t timeout_ticks) {
     __shared__ int s_ok;
@@ -43,15 +51,15 @@ __device__ __forceinline__ bool wait_counter(const uint32_t* counter, uint32_t t
                 }
             }
         }
-        if (ok)
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        else if (status)
+        if (ok) {
+            if constexpr (SYNC != FO_SYNC_COHERENT) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        } else if (status) {
             __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
         s_ok = ok;
     }
     __syncthreads();
-    // every wave invalidates its view before reading the group's data
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    if constexpr (SYNC == FO_SYNC_FENCE_ALL) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     return s_ok != 0;
 }
 
@@ -78,12 +86,12 @@ __device__ __forceinline__ uint16_t add1(uint16_t x, uint16_t y) {
     return (uint16_t)from_f32<DT>(to_f32<DT>(x) + to_f32<DT>(y));
 }
 
-// 16-byte path: src, peer and dst 16-byte aligned.
-template <int DT, bool SUM>
+// 16-byte path (FENCE_ALL / FENCE_ONE): src, peer and dst 16-byte aligned.
+template <int DT, bool SUM, int SYNC>
 __global__ __launch_bounds__(kThreads) void consume_vec_kernel(
     const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer, uint16_t* __restrict__ dst,
     int64_t len, const uint32_t* counter, uint32_t target, uint32_t* status, uint64_t timeout_ticks) {
-    if (counter && !wait_counter(counter, target, status, timeout_ticks)) return;
+    if (counter && !wait_counter<SYNC>(counter, target, status, timeout_ticks)) return;
     const int64_t n16 = len >> 3;
     const u32x4_t* s = reinterpret_cast<const u32x4_t*>(src);
     const u32x4_t* q = reinterpret_cast<const u32x4_t*>(peer);
@@ -115,40 +123,107 @@ __global__ __launch_bounds__(kThreads) void consume_vec_kernel(
     }
 }
 
-// Element path for unaligned buffers.
+// 8-byte path with device-coherent source loads (COHERENT): src, peer and
+// dst 8-byte aligned. Two 8-byte units per lane per unrolled step.
+template <int DT, bool SUM>
+__global__ __launch_bounds__(kThreads) void consume_coherent_kernel(
+    const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer, uint16_t* __restrict__ dst,
+    int64_t len, const uint32_t* counter, uint32_t target, uint32_t* status, uint64_t timeout_ticks) {
+    if (counter && !wait_counter<FO_SYNC_COHERENT>(counter, target, status, timeout_ticks)) return;
+    constexpr int U = 2 * kUnroll;
+    const int64_t n8 = len >> 2;
+    const uint64_t* s = reinterpret_cast<const uint64_t*>(src);
+    const uint64_t* q = reinterpret_cast<const uint64_t*>(peer);
+    uint64_t* d = reinterpret_cast<uint64_t*>(dst);
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    auto add4 = [](uint64_t x, uint64_t y) -> uint64_t {
+        u32x4_t a, b;
+        a[0] = (uint32_t)x; a[1] = (uint32_t)(x >> 32); a[2] = 0; a[3] = 0;
+        b[0] = (uint32_t)y; b[1] = (uint32_t)(y >> 32); b[2] = 0; b[3] = 0;
+        const u32x4_t r = add8<DT>(a, b);
+        return (uint64_t)r[0] | ((uint64_t)r[1] << 32);
+    };
+    for (; i + (U - 1) * stride < n8; i += U * stride) {
+        uint64_t x[U], y[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            x[u] = __hip_atomic_load(s + i + u * stride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if constexpr (SUM) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) y[u] = __builtin_nontemporal_load(q + i + u * stride);
+#pragma unroll
+            for (int u = 0; u < U; ++u) x[u] = add4(x[u], y[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) __builtin_nontemporal_store(x[u], d + i + u * stride);
+    }
+    for (; i < n8; i += stride) {
+        uint64_t x = __hip_atomic_load(s + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if constexpr (SUM) x = add4(x, __builtin_nontemporal_load(q + i));
+        __builtin_nontemporal_store(x, d + i);
+    }
+    // ragged tail (< 4 elements): an acquire, then plain 2-byte loads
+    if (blockIdx.x == 0 && threadIdx.x < (len & 3)) {
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        const int64_t e = (n8 << 2) + threadIdx.x;
+        dst[e] = SUM ? add1<DT>(src[e], peer[e]) : src[e];
+    }
+}
+
+// Element path for unaligned buffers: an acquire before plain loads (the
+// coherent mode falls back to FENCE_ONE here).
 template <int DT, bool SUM>
 __global__ __launch_bounds__(kThreads) void consume_elem_kernel(
     const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer, uint16_t* __restrict__ dst,
     int64_t len, const uint32_t* counter, uint32_t target, uint32_t* status, uint64_t timeout_ticks) {
-    if (counter && !wait_counter(counter, target, status, timeout_ticks)) return;
+    if (counter && !wait_counter<FO_SYNC_FENCE_ALL>(counter, target, status, timeout_ticks)) return;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
     for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < len; i += stride)
         dst[i] = SUM ? add1<DT>(src[i], peer[i]) : src[i];
 }
 
+template <int DT, bool SUM>
+void launch_variant(int sync, bool vec16, bool vec8, dim3 g, dim3 b, hipStream_t s, const uint16_t* src,
+                    const uint16_t* peer, uint16_t* dst, int64_t len, const uint32_t* counter,
+                    uint32_t target, uint32_t* status, uint64_t ticks) {
+    if (sync == FO_SYNC_COHERENT && vec8)
+        hipLaunchKernelGGL((consume_coherent_kernel<DT, SUM>), g, b, 0, s, src, peer, dst, len, counter,
+                           target, status, ticks);
+    else if (sync == FO_SYNC_FENCE_ALL && vec16)
+        hipLaunchKernelGGL((consume_vec_kernel<DT, SUM, FO_SYNC_FENCE_ALL>), g, b, 0, s, src, peer, dst,
+                           len, counter, target, status, ticks);
+    else if (vec16)
+        hipLaunchKernelGGL((consume_vec_kernel<DT, SUM, FO_SYNC_FENCE_ONE>), g, b, 0, s, src, peer, dst,
+                           len, counter, target, status, ticks);
+    else
+        hipLaunchKernelGGL((consume_elem_kernel<DT, SUM>), g, b, 0, s, src, peer, dst, len, counter,
+                           target, status, ticks);
+}
+
 }  // namespace
 
-hipError_t launch_consume(int dtype, const uint16_t* src, const uint16_t* peer, uint16_t* dst,
+hipError_t launch_consume(int dtype, int sync, const uint16_t* src, const uint16_t* peer, uint16_t* dst,
                           int64_t len, const uint32_t* counter, uint32_t target, uint32_t* status,
                           uint64_t timeout_ticks, hipStream_t s) {
-    const bool vec = ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst) |
-                       reinterpret_cast<uintptr_t>(peer)) & 15) == 0;
-    const int64_t work = vec ? (len >> 3) : len;
-    int64_t blocks = (work + (int64_t)kThreads * kUnroll - 1) / ((int64_t)kThreads * kUnroll);
+    const uintptr_t bits = reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst) |
+                           reinterpret_cast<uintptr_t>(peer);
+    const bool vec16 = (bits & 15) == 0, vec8 = (bits & 7) == 0;
+    const bool coherent = sync == FO_SYNC_COHERENT && vec8;
+    const int64_t per_block = coherent ? (int64_t)kThreads * 2 * kUnroll * 4
+                                       : vec16 ? (int64_t)kThreads * kUnroll * 8 : (int64_t)kThreads;
+    int64_t blocks = (len + per_block - 1) / per_block;
     if (blocks < 1) blocks = 1;
     if (blocks > kMaxConsumeBlocks) blocks = kMaxConsumeBlocks;
     const dim3 g((unsigned)blocks), b(kThreads);
     const bool sum = peer != nullptr;
-#define FO_CONSUME(KERN, DT, SUM) \
-    hipLaunchKernelGGL((KERN<DT, SUM>), g, b, 0, s, src, peer, dst, len, counter, target, status, timeout_ticks)
-    if (vec) {
-        if (dtype == FO_FP16) { if (sum) FO_CONSUME(consume_vec_kernel, FO_FP16, true); else FO_CONSUME(consume_vec_kernel, FO_FP16, false); }
-        else { if (sum) FO_CONSUME(consume_vec_kernel, FO_BF16, true); else FO_CONSUME(consume_vec_kernel, FO_BF16, false); }
+    if (dtype == FO_FP16) {
+        if (sum) launch_variant<FO_FP16, true>(sync, vec16, vec8, g, b, s, src, peer, dst, len, counter, target, status, timeout_ticks);
+        else launch_variant<FO_FP16, false>(sync, vec16, vec8, g, b, s, src, peer, dst, len, counter, target, status, timeout_ticks);
     } else {
-        if (dtype == FO_FP16) { if (sum) FO_CONSUME(consume_elem_kernel, FO_FP16, true); else FO_CONSUME(consume_elem_kernel, FO_FP16, false); }
-        else { if (sum) FO_CONSUME(consume_elem_kernel, FO_BF16, true); else FO_CONSUME(consume_elem_kernel, FO_BF16, false); }
+        if (sum) launch_variant<FO_BF16, true>(sync, vec16, vec8, g, b, s, src, peer, dst, len, counter, target, status, timeout_ticks);
+        else launch_variant<FO_BF16, false>(sync, vec16, vec8, g, b, s, src, peer, dst, len, counter, target, status, timeout_ticks);
     }
-#undef FO_CONSUME
     return hipGetLastError();
 }
 

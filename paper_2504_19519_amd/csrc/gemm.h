@@ -22,6 +22,7 @@ struct GemmArgs {
     const int32_t* pool_base;
     const int32_t* pool_off;
     uint32_t* counters;            // [P] or null
+    int32_t sync;                  // fo_sync_mode of the producer side
 };
 
 hipError_t launch_gemm(int dtype, int tile_m, int tile_n, const GemmArgs& a, int grid, hipStream_t s);

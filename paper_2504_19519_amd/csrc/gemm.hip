@@ -14,13 +14,13 @@
 //
 // Epilogue (Section 3.3 Approach; Section 3.2 Approach):
 //   1. accumulators -> fp16/bf16 (round to nearest even) -> LDS staging tile;
-//   2. every tile row goes out as full 16-byte stores to its destination:
+//   2. every tile row goes out as full-row stores to its destination:
 //      row-major C, the tile's slot (tile pattern), the slice's place in its
 //      group segment (subtile pattern) or the row's pool position (subtoken
 //      pattern);
-//   3. every wave makes its stores visible at agent scope (release fence),
-//      the workgroup meets at a barrier, and one lane adds 1 to the counter of
-//      the group that owns the slot.
+//   3. once the tile's stores are visible to all chiplets (fo_sync_mode:
+//      device-coherent stores + wait, or an agent-scope release), one lane
+//      adds 1 to the counter of the group that owns the slot.
 #include <hip/hip_runtime.h>
 
 #include "fo_device.h"
@@ -33,6 +33,9 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kBK = 64;
 constexpr int kLDK = kBK + 8;       // padded LDS row of an operand tile (halfs)
+// s_waitcnt operand with vmcnt = 0 and the other counters at their maximum
+// (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[5:4] at 15:14)
+constexpr int kWaitVmcnt0 = 0x0F70;
 
 template <int DT>
 __device__ __forceinline__ f32x16_t mfma32(u32x4_t a, u32x4_t b, f32x16_t c) {
@@ -50,12 +53,6 @@ struct Smem {
     static constexpr int kOperands = 2 * (kStageA + kStageB);
     static constexpr int kStaging = BM * kLDC;
     static constexpr int kHalfs = kOperands > kStaging ? kOperands : kStaging;
-};
-
-// Element offset, in C_out, of row r of this workgroup's tile.
-struct RowPlace {
-    int64_t base;        // offset of row 0 (row-major / tile / subtile)
-    int64_t stride;      // elements between consecutive rows
 };
 
 template <int DT, int BM, int BN, int WAVES_M, int WAVES_N>
@@ -202,6 +199,27 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
     }
     __syncthreads();
 
+    if (a.counters && a.sync == FO_SYNC_COHERENT) {
+        // Device-coherent 8-byte stores (written through to the point all
+        // chiplets share), each wave waits until its stores are complete,
+        // then one lane counts the tile: no cache write-back is needed.
+        constexpr int LPR = BN / 4;             // lanes per row (8 bytes each)
+        constexpr int RPI = 64 / LPR;           // rows per wave instruction
+        const int lr = lane / LPR, lc = lane % LPR;
+#pragma unroll 4
+        for (int r = wave * RPI + lr; r < BM; r += 4 * RPI) {
+            const uint64_t v = *reinterpret_cast<const uint64_t*>(Cs + r * S::kLDC + lc * 4);
+            __hip_atomic_store(reinterpret_cast<uint64_t*>(a.C + row_off[r]) + lc, v, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        __syncthreads();
+        if (tid == 0)
+            __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+
     constexpr int CPR = BN / 8;                 // 16-byte chunks per tile row
     constexpr int RPP = kThreads / CPR;         // rows per pass
     const int c = tid % CPR;
@@ -214,11 +232,20 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
     if (a.counters) {
         // Section 3.2: count the finished tile for its group once all of the
         // tile's stores are visible to every compute unit.
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-        __syncthreads();
-        if (tid == 0)
-            __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
+        if (a.sync == FO_SYNC_FENCE_ALL) {
+            // every wave: release fence at agent scope (L2 write-back + wait)
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            __syncthreads();
+            if (tid == 0)
+                __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            // workgroup barrier, then one release increment (one write-back)
+            __syncthreads();
+            if (tid == 0)
+                __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELEASE,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
 }
 

@@ -27,6 +27,14 @@ std::atomic<int64_t> g_timeout_us{[] {
     return (int64_t)2000000;
 }()};
 
+int env_mode(const char* name, int dflt) {
+    const char* e = std::getenv(name);
+    if (e && e[0] >= '0' && e[0] <= '2' && e[1] == '\0') return e[0] - '0';
+    return dflt;
+}
+std::atomic<int> g_sync_producer{env_mode("FO_SYNC_PRODUCER", FO_SYNC_COHERENT)};
+std::atomic<int> g_sync_consumer{env_mode("FO_SYNC_CONSUMER", FO_SYNC_COHERENT)};
+
 constexpr int kMaxDevices = 64;
 std::atomic<int64_t> g_clock_khz[kMaxDevices];   // 0 = unknown
 
@@ -97,6 +105,21 @@ void fo_set_poll_timeout_us(int64_t us) {
 }
 int64_t fo_get_poll_timeout_us(void) { return fo::poll_timeout_us(); }
 
+fo_status fo_set_sync_mode(int32_t producer, int32_t consumer) {
+    fo::clear_error();
+    if (producer < FO_SYNC_FENCE_ALL || producer > FO_SYNC_COHERENT || consumer < FO_SYNC_FENCE_ALL ||
+        consumer > FO_SYNC_COHERENT)
+        return fo::fail(FO_ERR_ARG, "sync modes are 0, 1 or 2");
+    fo::g_sync_producer.store(producer);
+    fo::g_sync_consumer.store(consumer);
+    return FO_OK;
+}
+
+void fo_get_sync_mode(int32_t* producer, int32_t* consumer) {
+    if (producer) *producer = fo::g_sync_producer.load();
+    if (consumer) *consumer = fo::g_sync_consumer.load();
+}
+
 fo_status fo_device_num_cus(int32_t device, int32_t* num_cus) {
     fo::clear_error();
     if (!num_cus) return fo::fail(FO_ERR_ARG, "num_cus is NULL");
@@ -150,6 +173,7 @@ fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan, cons
         a.pool_off = fo::dev_table<int32_t>(dev_plan, L.pool_off);
     }
     a.counters = plan->P > 0 ? counters : nullptr;
+    a.sync = fo::g_sync_producer.load(std::memory_order_relaxed);
     hipError_t e = fo::launch_gemm(plan->dtype, plan->tile_m, plan->tile_n, a, plan->tiles,
                                    (hipStream_t)stream);
     return e == hipSuccess ? FO_OK : fo::hip_fail("GEMM launch", e);
@@ -167,7 +191,8 @@ fo_status fo_consume_group(const void* src, const void* peer, void* dst, int64_t
     fo_status st = fo::clock_khz(&khz);
     if (st != FO_OK) return st;
     const uint64_t ticks = (uint64_t)fo::poll_timeout_us() * (uint64_t)khz / 1000u;
-    hipError_t e = fo::launch_consume(dtype, static_cast<const uint16_t*>(src),
+    hipError_t e = fo::launch_consume(dtype, fo::g_sync_consumer.load(std::memory_order_relaxed),
+                                      static_cast<const uint16_t*>(src),
                                       static_cast<const uint16_t*>(peer), static_cast<uint16_t*>(dst),
                                       len, counter, target, status_word, ticks, (hipStream_t)stream);
     return e == hipSuccess ? FO_OK : fo::hip_fail("consumer launch", e);

@@ -193,3 +193,21 @@ def test_consumers_wait_for_a_delayed_gemm():
     Cr = from_dev(C)[:w.M * w.N]
     ref = oracle.apply_consumer(o, Cr, inp.peer, w.dtype)
     np.testing.assert_array_equal(from_dev(dst)[:plan.dest_elems], ref)
+
+
+@pytest.mark.parametrize("producer", [0, 1, 2])
+@pytest.mark.parametrize("consumer", [0, 1, 2])
+@pytest.mark.parametrize("name", ["ar_2048x4096x4096", "rs_8192x8192x3584", "a2a_4096x7168x2048"])
+def test_sync_modes(producer, consumer, name):
+    # every producer x consumer publication scheme gives the same bits
+    old = fo.get_sync_mode()
+    fo.set_sync_mode(producer, consumer)
+    try:
+        M, N, K, cus, sizes = SMALL[name]
+        w = workloads.WORKLOADS[name].with_shape(M, N, K)
+        say(f"[sync modes] producer={producer} consumer={consumer} {w.name}")
+        inp = workloads.make_inputs(w)
+        plan, o = plan_for(w, inp, num_cus=cus, sizes=list(sizes))
+        check(w, inp, plan, o)
+    finally:
+        fo.set_sync_mode(*old)
