@@ -31,11 +31,18 @@ namespace fo {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kBK = 64;
-constexpr int kLDK = kBK + 8;       // padded LDS row of an operand tile (halfs)
-// s_waitcnt operand with vmcnt = 0 and the other counters at their maximum
+constexpr int kBK = 64;             // k values per main-loop step (128 bytes of fp16)
+constexpr int kStages = 3;          // LDS ring depth: loads run two steps ahead
+// s_waitcnt operand for vmcnt = vm and lgkmcnt = lgkm, expcnt at its maximum
 // (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[5:4] at 15:14)
-constexpr int kWaitVmcnt0 = 0x0F70;
+constexpr int wait_imm(int vm, int lgkm) {
+    return (vm & 15) | (7 << 4) | ((lgkm & 15) << 8) | (((vm >> 4) & 3) << 14);
+}
+constexpr int kWaitVmcnt0 = wait_imm(0, 15);
+// buffer resource word 3 for raw byte-addressed loads on gfx9
+constexpr int kRsrcWord3 = 0x00020000;
+
+typedef __attribute__((address_space(3))) void lds_void_t;
 
 template <int DT>
 __device__ __forceinline__ f32x16_t mfma32(u32x4_t a, u32x4_t b, f32x16_t c) {
@@ -45,29 +52,77 @@ __device__ __forceinline__ f32x16_t mfma32(u32x4_t a, u32x4_t b, f32x16_t c) {
         return __builtin_amdgcn_mfma_f32_32x32x16_bf16(bit_cast<bf16x8_t>(a), bit_cast<bf16x8_t>(b), c, 0, 0, 0);
 }
 
+// LDS plan of one workgroup. An operand tile row holds the 64 k values of
+// one row of A (or of W) = 128 bytes = 8 chunks of 16 bytes; chunk c of row
+// r is stored at slot c ^ (r % 8), so the 16-byte fragment reads of 8
+// consecutive rows at one k position hit 8 different slots.
 template <int BM, int BN>
-struct Smem {
-    static constexpr int kStageA = BM * kLDK;          // halfs
-    static constexpr int kStageB = BN * kLDK;
-    static constexpr int kLDC = BN + 8;
-    static constexpr int kOperands = 2 * (kStageA + kStageB);
-    static constexpr int kStaging = BM * kLDC;
-    static constexpr int kHalfs = kOperands > kStaging ? kOperands : kStaging;
+struct Tiles {
+    static constexpr int kRow = kBK * 2;
+    static constexpr int kA = BM * kRow, kB = BN * kRow;
+    static constexpr int kStage = kA + kB;
+    static constexpr int kLDC = BN + 8;                  // staging row (halfs)
+    static constexpr int kStaging = BM * kLDC * 2;
+    static constexpr int kAI = kA / 1024 / 4;            // 1 KB load blocks per wave
+    static constexpr int kBI = kB / 1024 / 4;
 };
+
+// Start loading one k step of this workgroup's A rows (into the first kA
+// bytes of `st`) and W rows (after them) with direct global-to-LDS loads:
+// each instruction moves 64 x 16 bytes into one 1 KB block. The rows are
+// addressed through buffer resources over the tile's row blocks (a_bytes and
+// w_bytes long; the host checks they fit in 32 bits), so a read past them
+// returns zero instead of faulting.
+template <int AI, int BI, int KA>
+__device__ __forceinline__ void issue_tile(const uint16_t* Ablk, const uint16_t* Wblk, uint32_t a_bytes,
+                                           uint32_t w_bytes, const uint32_t* voffA, const uint32_t* voffB,
+                                           uint32_t soff, char* st, int wave) {
+    const __amdgpu_buffer_rsrc_t rA =
+        __builtin_amdgcn_make_buffer_rsrc((void*)Ablk, 0, (int)a_bytes, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t rW =
+        __builtin_amdgcn_make_buffer_rsrc((void*)Wblk, 0, (int)w_bytes, kRsrcWord3);
+#pragma unroll
+    for (int i = 0; i < AI; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void_t*)(st + (wave * AI + i) * 1024), 16, voffA[i],
+                                                 soff, 0, 0);
+#pragma unroll
+    for (int i = 0; i < BI; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rW, (lds_void_t*)(st + KA + (wave * BI + i) * 1024), 16,
+                                                 voffB[i], soff, 0, 0);
+}
+
+// One main-loop synchronization: this wave waits until at most `vm` of its
+// vector memory operations are in flight (its part of the next tile has
+// landed in LDS) and until all of its LDS reads have returned (the stage it
+// read last can be refilled), then the workgroup meets at a barrier. The
+// empty asm statements keep the compiler from moving memory accesses (and
+// so the load issue order that the vmcnt count relies on) across this
+// point; the fence of __syncthreads() is not used because it would wait for
+// every in-flight operand load.
+template <int VM>
+__device__ __forceinline__ void wait_and_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(wait_imm(VM, 0));
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
 
 template <int DT, int BM, int BN, int WAVES_M, int WAVES_N>
 __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs a) {
     constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
     constexpr int MI = WTM / 32, NJ = WTN / 32;
-    constexpr int A_CH = BM * kBK / 8 / kThreads;      // 16-byte chunks per thread
-    constexpr int B_CH = BN * kBK / 8 / kThreads;
-    constexpr int ROWS_PER_LOAD = kThreads / (kBK / 8);
-    using S = Smem<BM, BN>;
+    using T = Tiles<BM, BN>;
     static_assert(WAVES_M * WAVES_N == kThreads / 64, "four waves");
     static_assert(WTM % 32 == 0 && WTN % 32 == 0, "32x32 MFMA blocks");
-    static_assert(A_CH >= 1 && B_CH >= 1, "tile too small for the loader");
+    static_assert(T::kAI >= 1 && T::kBI >= 1 && T::kA % 4096 == 0 && T::kB % 4096 == 0,
+                  "each wave loads whole 1 KB blocks");
+    static_assert(T::kStaging <= 2 * T::kStage, "output staging fits in two stages");
 
-    __shared__ __attribute__((aligned(16))) uint16_t smem[S::kHalfs];
+    // Three stages in separate arrays, so that the compiler can tell the
+    // stage being read from the stages being filled.
+    __shared__ __attribute__((aligned(1024))) char st0[T::kStage];
+    __shared__ __attribute__((aligned(1024))) char st1[T::kStage];
+    __shared__ __attribute__((aligned(1024))) char st2[T::kStage];
     __shared__ int64_t row_off[BM];
 
     const int tid = threadIdx.x;
@@ -87,29 +142,21 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
         rank = a.row_rank[tm * BM + tid];
     }
 
-    const uint16_t* Ag = a.A + (int64_t)tm * BM * K;
-    const uint16_t* Wg = a.W + (int64_t)tn * BN * K;
-    const int lrow = tid / (kBK / 8), lkc = tid % (kBK / 8);
-
-    u32x4_t ra[A_CH], rb[B_CH];
-    auto gload = [&](int kt) {
-        const int64_t k0 = (int64_t)kt * kBK + lkc * 8;
+    // A load instruction fills one 1 KB block = 8 rows: lane l writes slot
+    // l % 8 of row l / 8, so it fetches chunk (l % 8) ^ (l / 8) of that row.
+    const uint32_t lane_chunk = 16u * (uint32_t)((lane & 7) ^ (lane >> 3));
+    uint32_t voffA[T::kAI], voffB[T::kBI];
 #pragma unroll
-        for (int i = 0; i < A_CH; ++i)
-            ra[i] = *reinterpret_cast<const u32x4_t*>(Ag + (int64_t)(lrow + ROWS_PER_LOAD * i) * K + k0);
+    for (int i = 0; i < T::kAI; ++i)
+        voffA[i] = (uint32_t)(((wave * T::kAI + i) * 8 + (lane >> 3)) * K * 2) + lane_chunk;
 #pragma unroll
-        for (int i = 0; i < B_CH; ++i)
-            rb[i] = *reinterpret_cast<const u32x4_t*>(Wg + (int64_t)(lrow + ROWS_PER_LOAD * i) * K + k0);
-    };
-    auto sstore = [&](int stage) {
-        uint16_t* As = smem + stage * S::kStageA;
-        uint16_t* Bs = smem + 2 * S::kStageA + stage * S::kStageB;
-#pragma unroll
-        for (int i = 0; i < A_CH; ++i)
-            *reinterpret_cast<u32x4_t*>(As + (lrow + ROWS_PER_LOAD * i) * kLDK + lkc * 8) = ra[i];
-#pragma unroll
-        for (int i = 0; i < B_CH; ++i)
-            *reinterpret_cast<u32x4_t*>(Bs + (lrow + ROWS_PER_LOAD * i) * kLDK + lkc * 8) = rb[i];
+    for (int i = 0; i < T::kBI; ++i)
+        voffB[i] = (uint32_t)(((wave * T::kBI + i) * 8 + (lane >> 3)) * K * 2) + lane_chunk;
+    const uint16_t* Ablk = a.A + (int64_t)tm * BM * K;
+    const uint16_t* Wblk = a.W + (int64_t)tn * BN * K;
+    auto issue = [&](int kt, char* st) {
+        issue_tile<T::kAI, T::kBI, T::kA>(Ablk, Wblk, (uint32_t)(BM * K * 2), (uint32_t)(BN * K * 2),
+                                         voffA, voffB, (uint32_t)kt * (kBK * 2), st, wave);
     };
 
     f32x16_t acc[MI][NJ];
@@ -120,30 +167,31 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    const int KT = (int)(K / kBK);
-    if (KT > 0) {
-        gload(0);
-        sstore(0);
-    }
-    __syncthreads();
-
     // Fragment addressing: lane l feeds row (l % 32) of a 32-row block with
-    // the 8 consecutive k values starting at 8 * (l / 32) of a 16-wide step.
-    const int frag = (lane & 31) * kLDK + (lane >> 5) * 8;
-    for (int kt = 0; kt < KT; ++kt) {
-        const int cur = kt & 1;
-        if (kt + 1 < KT) gload(kt + 1);
-        const uint16_t* As = smem + cur * S::kStageA + wm * WTM * kLDK + frag;
-        const uint16_t* Bs = smem + 2 * S::kStageA + cur * S::kStageB + wn * WTN * kLDK + frag;
+    // the 8 consecutive k values of chunk 2*kk + l/32 of the 16-wide step kk.
+    const int a_row = (wm * WTM + (lane & 31)) * T::kRow;
+    const int b_row = T::kA + (wn * WTN + (lane & 31)) * T::kRow;
+    int cslot[kBK / 16];
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) cslot[kk] = 16 * ((2 * kk + (lane >> 5)) ^ (lane & 7));
+
+    const int KT = (int)(K / kBK);
+    // One main-loop step: wait for tile kt (tile kt+1 may still be loading),
+    // meet at the barrier (everyone is also done with the stage about to be
+    // refilled), start tile kt+2, multiply tile kt.
+    auto step = [&](int kt, const char* cur, char* nxt) {
+        if (kt + 1 < KT) wait_and_barrier<T::kAI + T::kBI>();
+        else wait_and_barrier<0>();
+        if (kt + 2 < KT) issue(kt + 2, nxt);
 #pragma unroll
         for (int kk = 0; kk < kBK / 16; ++kk) {
             u32x4_t af[MI], bf[NJ];
 #pragma unroll
             for (int i = 0; i < MI; ++i)
-                af[i] = *reinterpret_cast<const u32x4_t*>(As + i * 32 * kLDK + kk * 16);
+                af[i] = *reinterpret_cast<const u32x4_t*>(cur + a_row + i * 32 * T::kRow + cslot[kk]);
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
-                bf[j] = *reinterpret_cast<const u32x4_t*>(Bs + j * 32 * kLDK + kk * 16);
+                bf[j] = *reinterpret_cast<const u32x4_t*>(cur + b_row + j * 32 * T::kRow + cslot[kk]);
             // W fragment as the MFMA's first operand: the 32x32 result block
             // is C^T, so each lane holds 4 consecutive output columns.
 #pragma unroll
@@ -152,9 +200,19 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
                 for (int j = 0; j < NJ; ++j)
                     acc[i][j] = mfma32<DT>(bf[j], af[i], acc[i][j]);
         }
-        if (kt + 1 < KT) sstore(cur ^ 1);
-        __syncthreads();
+    };
+
+    if (KT > 0) issue(0, st0);
+    if (KT > 1) issue(1, st1);
+    int kt = 0;
+    for (; kt + 3 <= KT; kt += 3) {      // tile t lives in stage t % 3
+        step(kt, st0, st2);
+        step(kt + 1, st1, st0);
+        step(kt + 2, st2, st1);
     }
+    if (kt < KT) step(kt, st0, st2);
+    if (kt + 1 < KT) step(kt + 1, st1, st0);
+    __syncthreads();     // operand stages are reused for the output tile
 
     // ---- epilogue -------------------------------------------------------
     // Destination of row `tid` of the tile, by pattern.
@@ -179,9 +237,11 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
         row_off[r] = off;
     }
 
-    // accumulators -> LDS staging [BM][BN + 8] (operand buffers are free:
-    // the loop ended with a barrier)
-    uint16_t* Cs = smem;
+    // accumulators -> LDS staging [BM][BN + 8], rows [0, BM/2) in stage 0
+    // and [BM/2, BM) in stage 1 (the loop ended with a barrier)
+    auto crow = [&](int r) -> uint16_t* {
+        return reinterpret_cast<uint16_t*>(r < BM / 2 ? st0 + r * T::kLDC * 2 : st1 + (r - BM / 2) * T::kLDC * 2);
+    };
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
         const int m = wm * WTM + i * 32 + (lane & 31);
@@ -193,7 +253,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
                 u32x2_t v;
                 v[0] = pack2<DT>(acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]);
                 v[1] = pack2<DT>(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-                *reinterpret_cast<u32x2_t*>(Cs + m * S::kLDC + n) = v;
+                *reinterpret_cast<u32x2_t*>(crow(m) + n) = v;
             }
         }
     }
@@ -208,7 +268,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
         const int lr = lane / LPR, lc = lane % LPR;
 #pragma unroll 4
         for (int r = wave * RPI + lr; r < BM; r += 4 * RPI) {
-            const uint64_t v = *reinterpret_cast<const uint64_t*>(Cs + r * S::kLDC + lc * 4);
+            const uint64_t v = *reinterpret_cast<const uint64_t*>(crow(r) + lc * 4);
             __hip_atomic_store(reinterpret_cast<uint64_t*>(a.C + row_off[r]) + lc, v, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
         }
@@ -225,7 +285,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
     const int c = tid % CPR;
 #pragma unroll 4
     for (int r = tid / CPR; r < BM; r += RPP) {
-        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(Cs + r * S::kLDC + c * 8);
+        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(crow(r) + c * 8);
         *reinterpret_cast<u32x4_t*>(a.C + row_off[r] + c * 8) = v;
     }
 
