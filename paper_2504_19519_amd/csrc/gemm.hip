@@ -6,11 +6,12 @@
 // one tile per compute unit (Section 2.1.1) and position p is the tile's slot
 // in the reordered output (Section 3.3 Approach (1)).
 //
-// Main loop: MFMA v_mfma_f32_32x32x16 (fp16 / bf16 in, fp32 accumulate),
-// A and B tiles of BK = 64 double-buffered in LDS with padded rows (conflict
-// free 16-byte fragment reads), the next K block prefetched into registers
-// while the current one is multiplied. The main loop is the same for every
-// output pattern (Section 5: only the epilogue changes).
+// Main loop: MFMA v_mfma_f32_32x32x16 (fp16 / bf16 in, fp32 accumulate) on
+// k steps of 64. A and W tiles move from HBM straight into a 3-stage LDS ring
+// (direct global-to-LDS loads, XOR-swizzled rows for conflict-free 16-byte
+// fragment reads), issued three steps ahead; fragments of the next 16-wide
+// k step are read while the MFMAs of the current one run. The main loop is
+// the same for every output pattern (Section 5: only the epilogue changes).
 //
 // Epilogue (Section 3.3 Approach; Section 3.2 Approach):
 //   1. accumulators -> fp16/bf16 (round to nearest even) -> LDS staging tile;
@@ -154,9 +155,15 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
         voffB[i] = (uint32_t)(((wave * T::kBI + i) * 8 + (lane >> 3)) * K * 2) + lane_chunk;
     const uint16_t* Ablk = a.A + (int64_t)tm * BM * K;
     const uint16_t* Wblk = a.W + (int64_t)tn * BN * K;
+    const int KT = (int)(K / kBK);
+    // Tiles past the last k step are "loaded" through empty resources: the
+    // loads return zeros without touching memory, so every step issues the
+    // same loads and the wait counts stay uniform (no branches).
     auto issue = [&](int kt, char* st) {
-        issue_tile<T::kAI, T::kBI, T::kA>(Ablk, Wblk, (uint32_t)(BM * K * 2), (uint32_t)(BN * K * 2),
-                                         voffA, voffB, (uint32_t)kt * (kBK * 2), st, wave);
+        const bool live = kt < KT;
+        issue_tile<T::kAI, T::kBI, T::kA>(Ablk, Wblk, live ? (uint32_t)(BM * K * 2) : 0u,
+                                         live ? (uint32_t)(BN * K * 2) : 0u, voffA, voffB,
+                                         live ? (uint32_t)kt * (kBK * 2) : 0u, st, wave);
     };
 
     f32x16_t acc[MI][NJ];
@@ -175,43 +182,66 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) cslot[kk] = 16 * ((2 * kk + (lane >> 5)) ^ (lane & 7));
 
-    const int KT = (int)(K / kBK);
-    // One main-loop step: wait for tile kt (tile kt+1 may still be loading),
-    // meet at the barrier (everyone is also done with the stage about to be
-    // refilled), start tile kt+2, multiply tile kt.
-    auto step = [&](int kt, const char* cur, char* nxt) {
-        if (kt + 1 < KT) wait_and_barrier<T::kAI + T::kBI>();
-        else wait_and_barrier<0>();
-        if (kt + 2 < KT) issue(kt + 2, nxt);
+    // Two fragment register sets: the fragments of k step kk+1 are read from
+    // LDS while the MFMAs of k step kk run.
+    u32x4_t fa0[MI], fb0[NJ], fa1[MI], fb1[NJ];
+    auto load_frags = [&](const char* st, int kk, u32x4_t (&fa)[MI], u32x4_t (&fb)[NJ]) {
 #pragma unroll
-        for (int kk = 0; kk < kBK / 16; ++kk) {
-            u32x4_t af[MI], bf[NJ];
+        for (int i = 0; i < MI; ++i)
+            fa[i] = *reinterpret_cast<const u32x4_t*>(st + a_row + i * 32 * T::kRow + cslot[kk]);
 #pragma unroll
-            for (int i = 0; i < MI; ++i)
-                af[i] = *reinterpret_cast<const u32x4_t*>(cur + a_row + i * 32 * T::kRow + cslot[kk]);
+        for (int j = 0; j < NJ; ++j)
+            fb[j] = *reinterpret_cast<const u32x4_t*>(st + b_row + j * 32 * T::kRow + cslot[kk]);
+    };
+    // W fragment as the MFMA's first operand: the 32x32 result block is C^T,
+    // so each lane holds 4 consecutive output columns.
+    auto mma = [&](const u32x4_t (&fa)[MI], const u32x4_t (&fb)[NJ]) {
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
-                bf[j] = *reinterpret_cast<const u32x4_t*>(cur + b_row + j * 32 * T::kRow + cslot[kk]);
-            // W fragment as the MFMA's first operand: the 32x32 result block
-            // is C^T, so each lane holds 4 consecutive output columns.
-#pragma unroll
-            for (int i = 0; i < MI; ++i)
-#pragma unroll
-                for (int j = 0; j < NJ; ++j)
-                    acc[i][j] = mfma32<DT>(bf[j], af[i], acc[i][j]);
-        }
+                acc[i][j] = mfma32<DT>(fb[j], fa[i], acc[i][j]);
     };
 
-    if (KT > 0) issue(0, st0);
-    if (KT > 1) issue(1, st1);
+    // Step kt multiplies the tile in stage `cur` (its k step 0 fragments are
+    // already in fa0/fb0). Before its last k step, every wave has read all of
+    // `cur` and tile kt+1 has landed: after the barrier, tile kt+3 goes into
+    // `cur` and the first fragments of tile kt+1 (stage `nxt`) are read while
+    // the last MFMAs of tile kt run.
+    auto step = [&](int kt, char* cur, const char* nxt) {
+        load_frags(cur, 1, fa1, fb1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(fa0, fb0);
+        __builtin_amdgcn_sched_barrier(0);
+        load_frags(cur, 2, fa0, fb0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(fa1, fb1);
+        __builtin_amdgcn_sched_barrier(0);
+        load_frags(cur, 3, fa1, fb1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(fa0, fb0);
+        wait_and_barrier<T::kAI + T::kBI>();
+        issue(kt + 3, cur);
+        load_frags(nxt, 0, fa0, fb0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(fa1, fb1);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    issue(0, st0);
+    issue(1, st1);
+    issue(2, st2);
+    wait_and_barrier<2 * (T::kAI + T::kBI)>();
+    load_frags(st0, 0, fa0, fb0);
     int kt = 0;
     for (; kt + 3 <= KT; kt += 3) {      // tile t lives in stage t % 3
-        step(kt, st0, st2);
-        step(kt + 1, st1, st0);
-        step(kt + 2, st2, st1);
+        step(kt, st0, st1);
+        step(kt + 1, st1, st2);
+        step(kt + 2, st2, st0);
     }
-    if (kt < KT) step(kt, st0, st2);
-    if (kt + 1 < KT) step(kt + 1, st1, st0);
+    if (kt < KT) step(kt, st0, st1);
+    if (kt + 1 < KT) step(kt + 1, st1, st2);
+    wait_and_barrier<0>();    // no load may still be writing LDS
     __syncthreads();     // operand stages are reused for the output tile
 
     // ---- epilogue -------------------------------------------------------

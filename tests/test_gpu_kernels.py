@@ -60,6 +60,19 @@ def test_plain_gemm_matches_oracle(dtype, tile, shape):
     assert_close_bits(C, oracle.gemm_ref(A, W, dtype).reshape(-1), dtype, "plain GEMM")
 
 
+@pytest.mark.parametrize("K", [64 * kt for kt in range(1, 10)] + [64 * 56])
+@pytest.mark.parametrize("tile", [(256, 128), (64, 64)])
+def test_gemm_every_k_step_count(K, tile):
+    # the main loop runs k steps in groups of three; cover every remainder
+    M, N = 2 * tile[0], 3 * tile[1]
+    say(f"[gemm k sweep] tile={tile} K={K}")
+    A, W = _operands(M, N, K, "fp16", 15 + K)
+    plan = fo.plan_groups(M, N, K, tile_m=tile[0], tile_n=tile[1], order="xcd", num_cus=4,
+                          pattern="rowmajor", sizes=[2])
+    C = _gemm(plan, A, W, poison="fp16")
+    assert_close_bits(C, oracle.gemm_ref(A, W, "fp16").reshape(-1), "fp16", f"GEMM K={K}")
+
+
 @pytest.mark.parametrize("dtype", ["fp16", "bf16"])
 @pytest.mark.parametrize("tile", [(256, 128), (64, 64)])
 def test_identity_operand_is_exact(dtype, tile):
