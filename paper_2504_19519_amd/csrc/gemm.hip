@@ -55,8 +55,11 @@ __device__ __forceinline__ f32x16_t mfma32(u32x4_t a, u32x4_t b, f32x16_t c) {
 
 // LDS plan of one workgroup. An operand tile row holds the 64 k values of
 // one row of A (or of W) = 128 bytes = 8 chunks of 16 bytes; chunk c of row
-// r is stored at slot c ^ (r % 8), so the 16-byte fragment reads of 8
-// consecutive rows at one k position hit 8 different slots.
+// r is stored at slot c ^ ((r / 2) % 8). The gfx950 LDS serves a 16-byte
+// read for 16 lanes per cycle across 64 banks (256 bytes): rows r and r+1
+// share a 256-byte bank line, so the 16 rows read together at one k position
+// must land in 16 different (row parity, slot) pairs, which this swizzle
+// gives for any 16 consecutive rows.
 template <int BM, int BN>
 struct Tiles {
     static constexpr int kRow = kBK * 2;
@@ -90,6 +93,21 @@ __device__ __forceinline__ void issue_tile(const uint16_t* Ablk, const uint16_t*
     for (int i = 0; i < BI; ++i)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rW, (lds_void_t*)(st + KA + (wave * BI + i) * 1024), 16,
                                                  voffB[i], soff, 0, 0);
+}
+
+// Instruction order inside one k-step phase of the main loop: each MFMA
+// (32 cycles of matrix work) carries one LDS fragment read and, in the last
+// phase, up to DPM direct-to-LDS load issues in its shadow, so the matrix
+// pipe does not drain while reads and loads are issued.
+template <int MFMA, int READS, int DMA, int DPM>
+__device__ __forceinline__ void interleave_phase() {
+#pragma unroll
+    for (int i = 0; i < MFMA; ++i) {
+        if (i < READS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);          // LDS read
+        if (DPM > 0 && i * DPM < DMA) __builtin_amdgcn_sched_group_barrier(0x020, DPM, 0);  // VMEM
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                         // MFMA
+    }
+    if (READS > MFMA) __builtin_amdgcn_sched_group_barrier(0x100, READS - MFMA, 0);
 }
 
 // One main-loop synchronization: this wave waits until at most `vm` of its
@@ -144,15 +162,17 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
     }
 
     // A load instruction fills one 1 KB block = 8 rows: lane l writes slot
-    // l % 8 of row l / 8, so it fetches chunk (l % 8) ^ (l / 8) of that row.
-    const uint32_t lane_chunk = 16u * (uint32_t)((lane & 7) ^ (lane >> 3));
+    // l % 8 of row r = 8 * block + l / 8, so it fetches chunk
+    // (l % 8) ^ ((r / 2) % 8) of that row.
+    auto voff = [&](int blk) -> uint32_t {
+        const int r = blk * 8 + (lane >> 3);
+        return (uint32_t)(r * K * 2) + 16u * (uint32_t)((lane & 7) ^ ((r >> 1) & 7));
+    };
     uint32_t voffA[T::kAI], voffB[T::kBI];
 #pragma unroll
-    for (int i = 0; i < T::kAI; ++i)
-        voffA[i] = (uint32_t)(((wave * T::kAI + i) * 8 + (lane >> 3)) * K * 2) + lane_chunk;
+    for (int i = 0; i < T::kAI; ++i) voffA[i] = voff(wave * T::kAI + i);
 #pragma unroll
-    for (int i = 0; i < T::kBI; ++i)
-        voffB[i] = (uint32_t)(((wave * T::kBI + i) * 8 + (lane >> 3)) * K * 2) + lane_chunk;
+    for (int i = 0; i < T::kBI; ++i) voffB[i] = voff(wave * T::kBI + i);
     const uint16_t* Ablk = a.A + (int64_t)tm * BM * K;
     const uint16_t* Wblk = a.W + (int64_t)tn * BN * K;
     const int KT = (int)(K / kBK);
@@ -180,7 +200,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
     const int b_row = T::kA + (wn * WTN + (lane & 31)) * T::kRow;
     int cslot[kBK / 16];
 #pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) cslot[kk] = 16 * ((2 * kk + (lane >> 5)) ^ (lane & 7));
+    for (int kk = 0; kk < kBK / 16; ++kk) cslot[kk] = 16 * ((2 * kk + (lane >> 5)) ^ ((lane >> 1) & 7));
 
     // Two fragment register sets: the fragments of k step kk+1 are read from
     // LDS while the MFMAs of k step kk run.
@@ -208,23 +228,32 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
     // `cur` and tile kt+1 has landed: after the barrier, tile kt+3 goes into
     // `cur` and the first fragments of tile kt+1 (stage `nxt`) are read while
     // the last MFMAs of tile kt run.
+    constexpr int kMfma = MI * NJ, kReads = MI + NJ, kDma = T::kAI + T::kBI;
+    constexpr int kDmaPerMfma = (kDma + kMfma - 1) / kMfma;
+
+    // Step kt multiplies the tile in stage `cur` (its k step 0 fragments are
+    // already in fa0/fb0). Before its last k step, every wave has read all of
+    // `cur` and tile kt+1 has landed: after the barrier, tile kt+3 goes into
+    // `cur` and the first fragments of tile kt+1 (stage `nxt`) are read while
+    // the last MFMAs of tile kt run.
     auto step = [&](int kt, char* cur, const char* nxt) {
         load_frags(cur, 1, fa1, fb1);
-        __builtin_amdgcn_sched_barrier(0);
         mma(fa0, fb0);
+        interleave_phase<kMfma, kReads, 0, 0>();
         __builtin_amdgcn_sched_barrier(0);
         load_frags(cur, 2, fa0, fb0);
-        __builtin_amdgcn_sched_barrier(0);
         mma(fa1, fb1);
+        interleave_phase<kMfma, kReads, 0, 0>();
         __builtin_amdgcn_sched_barrier(0);
         load_frags(cur, 3, fa1, fb1);
-        __builtin_amdgcn_sched_barrier(0);
         mma(fa0, fb0);
+        interleave_phase<kMfma, kReads, 0, 0>();
+        __builtin_amdgcn_sched_barrier(0);
         wait_and_barrier<T::kAI + T::kBI>();
         issue(kt + 3, cur);
         load_frags(nxt, 0, fa0, fb0);
-        __builtin_amdgcn_sched_barrier(0);
         mma(fa1, fb1);
+        interleave_phase<kMfma, kReads, kDma, kDmaPerMfma>();
         __builtin_amdgcn_sched_barrier(0);
     };
 
