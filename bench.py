@@ -228,6 +228,18 @@ def main():
 
     # ---- components alone ------------------------------------------------
     res = {}
+    if args.phase == "step":
+        # profiler run: only identical overlapped steps (one group per wave
+        # unless --sizes), so per-kernel averages match the live timing
+        sizes = [int(x) for x in args.sizes.split(",")] if args.sizes else [1] * T
+        plan = make_plan(w, inp, num_cus, sizes=sizes)
+        dp = dev_plan(torch, plan)
+        torch.cuda.synchronize()
+        step_us, gemm_mean_us, gemm_med_us, wall = timed_steps(torch, w, plan, dp, b, s1, s2, args.steps,
+                                                               args.warmup)
+        print(json.dumps({"phase": "step", "groups": sizes, "step_us": round(step_us, 2),
+                          "gemm_us": round(gemm_mean_us, 2), "gemm_tflops": round(flops / gemm_mean_us / 1e6, 2)}))
+        return
     if args.phase == "all":
         log("plain GEMM / signaled GEMM")
         plain_us = time_loop(torch, lambda: fo.gemm_signal_reorder(plan_rm, None, b.A, b.W, b.C, None, s1),
@@ -241,10 +253,6 @@ def main():
         cons_all_us = ys[-1]
         res.update(plain_us=plain_us, sig_us=sig_us, cons_all_us=cons_all_us,
                    cons_gbs=cons_bytes_per_elem * n_all / cons_all_us / 1e3, curve=(xs, ys))
-    else:
-        sig_us = time_loop(torch, lambda: fo.gemm_signal_reorder(base_plan, dp_base, b.A, b.W, b.C, b.counters, s1),
-                           5, 2, s1)
-        xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N)
 
     # ---- the plan: explicit, or Algorithm 1 on the measured inputs ---------
     if args.sizes:
@@ -259,9 +267,6 @@ def main():
     log(f"timed steps: warmup {args.warmup}, steps {args.steps}")
     step_us, gemm_mean_us, gemm_med_us, wall = timed_steps(torch, w, plan, dp, b, s1, s2, args.steps,
                                                            args.warmup)
-    if args.phase == "step":
-        print(json.dumps({"phase": "step", "step_us": step_us, "gemm_us": gemm_mean_us}))
-        return
     serial_us, serial_gemm_us, _, _ = timed_steps(torch, w, plan, dp, b, s1, s1, args.steps, args.warmup)
 
     # ---- group-size sweep (waves per group) ---------------------------------
