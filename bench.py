@@ -22,6 +22,7 @@ sample of output rows.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import math
 import os
@@ -54,6 +55,9 @@ def parse():
     ap.add_argument("--phase", default="all", choices=["all", "step", "gemm", "copy"],
                     help="step/gemm/copy run only that loop (for profiler runs)")
     ap.add_argument("--sizes", default=None, help="explicit partition in waves, e.g. 1,1,2,4")
+    ap.add_argument("--tile", default=None, help="override the workload's output tile, e.g. 256x256")
+    ap.add_argument("--consumer-blocks", type=int, default=None,
+                    help="cap of every consumer launch's grid (1..256)")
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
@@ -198,7 +202,12 @@ def main():
     torch.cuda.set_device(0)
     fo.lib()
     w = workloads.WORKLOADS[args.workload]
+    if args.tile:
+        tm, tn = (int(x) for x in args.tile.lower().split("x"))
+        w = dataclasses.replace(w, tile_m=tm, tile_n=tn)
     log(f"workload {w.name}: M={w.M} N={w.N} K={w.K} {w.dtype} pattern={w.pattern}")
+    if args.consumer_blocks:
+        fo.set_consumer_blocks(args.consumer_blocks)
     inp = workloads.make_inputs(w)
     num_cus = fo.device_num_cus(0)
     tiles = (w.M // w.tile_m) * (w.N // w.tile_n)
@@ -293,6 +302,15 @@ def main():
                                       "overlapped_gemm_us": round(gm, 2)}
     fo.set_sync_mode(*default_modes)
 
+    # ---- consumer grid size (fo_set_consumer_blocks) ------------------------
+    grid_variants = {}
+    default_blocks = fo.get_consumer_blocks()
+    for nb in (16, 32, 64, 128, 256):
+        fo.set_consumer_blocks(nb)
+        us, gm, _, _ = timed_steps(torch, w, plan, dp, b, s1, s2, max(10, args.steps // 2), 3)
+        grid_variants[str(nb)] = {"overlapped_step_us": round(us, 2), "overlapped_gemm_us": round(gm, 2)}
+    fo.set_consumer_blocks(default_blocks)
+
     # ---- consistency at full size: overlapped vs serialized output bits ----
     run_step(torch, w, plan, dp, b, s1, s1)
     torch.cuda.synchronize()
@@ -365,6 +383,7 @@ def main():
         "sweep_waves_per_group": sweep,
         "sync_modes": {"default": list(default_modes), "variants": sync_variants,
                        "overlapped_equals_serial_bits": consistent},
+        "consumer_blocks": {"default": default_blocks, "variants": grid_variants},
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
     }

@@ -89,7 +89,7 @@ typedef enum { FO_UNIT_WAVES = 0, FO_UNIT_TILES = 1 } fo_unit;
 typedef struct {
     int64_t M, N, K;          /* C[M,N] = A[M,K] x B[K,N] (Section 2.1.1)          */
     int32_t dtype;            /* fo_dtype of A, B, C                                */
-    int32_t tile_m, tile_n;   /* output tile; kernels exist for 256x128 and 64x64   */
+    int32_t tile_m, tile_n;   /* output tile; GEMM kernels: 256x128, 256x256, 64x64 */
     int32_t order;            /* fo_order                                           */
     int32_t group_m;          /* band height for GROUPED / XCD (>= 1)               */
     int32_t num_xcds;         /* chiplets for XCD (>= 1)                            */
@@ -194,7 +194,8 @@ fo_status fo_plan_to_device(const fo_plan* plan, void* dev_buf, size_t bytes, vo
  * reorder sits in the epilogue, the main loop is untouched).
  *
  * A: [M, K] row-major. W: B^T, [N, K] row-major (K contiguous, the weight
- * layout of a linear layer). K must be a multiple of 64; A, W, C_out 16-byte
+ * layout of a linear layer). K must be a multiple of 64 and max(tile_m,
+ * tile_n) * K * 2 must not exceed 2^31 - 1; A, W, C_out 16-byte
  * aligned. C_out by pattern:
  *   ROWMAJOR: [M, N] row-major.
  *   TILE:     [tiles*tile_m, tile_n] row-major; slot s holds the tile at rows
@@ -265,8 +266,13 @@ fo_status fo_reset_counters(uint32_t* counters, int32_t n, void* stream);
  * One overlapped run of the whole path (Section 5: GEMM on one stream, the
  * signalling + communication on another; Figure 5 order):
  *   gemm_stream: reset counters + status -> event E0 -> GEMM (signalling)
- *   comm_stream: wait E0 -> fo_consume_group for every plan segment -> event E1
+ *   comm_stream: wait E0 -> one consumer launch per group -> event E1
  *   gemm_stream: wait E1 -> fo_post_reorder (if out != NULL)
+ * A group's consumer launch waits once for the group's counter and then
+ * does what fo_consume_group does for each of the group's plan segments
+ * (fo_plan_segments: 1, R or B of them). Every group but the last uses at
+ * most fo_get_consumer_blocks() workgroups; the last group, which runs
+ * after the GEMM, uses up to 256.
  * With comm_stream == gemm_stream (or NULL) the same work runs serialized.
  * Buffers: C_out (GEMM output, see fo_gemm_signal_reorder), peer (NULL for
  * All-to-All; else the peer's partial in C_out's layout), dst
@@ -305,6 +311,15 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan,
 typedef enum { FO_SYNC_FENCE_ALL = 0, FO_SYNC_FENCE_ONE = 1, FO_SYNC_COHERENT = 2 } fo_sync_mode;
 fo_status fo_set_sync_mode(int32_t producer, int32_t consumer);
 void fo_get_sync_mode(int32_t* producer, int32_t* consumer);
+
+/* Largest grid of a consumer launch that runs beside the GEMM (every
+ * fo_consume_group call, and every group but the last in
+ * fo_run_overlapped), in 256-thread workgroups (1 .. 256, default 256; env
+ * FO_CONSUMER_BLOCKS overrides at load time). Fewer workgroups stream a
+ * group more slowly but leave more of the memory system to the GEMM.
+ * Process-wide; FO_ERR_ARG outside the range. */
+fo_status fo_set_consumer_blocks(int32_t max_blocks);
+int32_t fo_get_consumer_blocks(void);
 
 /* Upper bound of one consumer wait, in microseconds (default 2 s; env
  * FO_POLL_TIMEOUT_US overrides at load time). */

@@ -20,7 +20,8 @@ import numpy as np
 __all__ = [
     "FoError", "Plan", "plan_groups", "gemm_signal_reorder", "consume_group",
     "post_reorder", "reset_counters", "run_overlapped", "set_poll_timeout_us",
-    "get_poll_timeout_us", "device_num_cus", "set_sync_mode", "get_sync_mode", "LIB_PATH",
+    "get_poll_timeout_us", "device_num_cus", "set_sync_mode", "get_sync_mode",
+    "set_consumer_blocks", "get_consumer_blocks", "LIB_PATH",
     "FP16", "BF16", "TILE", "SUBTILE", "SUBTOKEN", "ROWMAJOR",
 ]
 
@@ -101,6 +102,8 @@ def lib() -> ctypes.CDLL:
                                     vp, vp, vp, vp, vp, vp]
     L.fo_set_sync_mode.argtypes, L.fo_set_sync_mode.restype = [i32, i32], ctypes.c_int
     L.fo_get_sync_mode.argtypes = [pi32, pi32]
+    L.fo_set_consumer_blocks.argtypes, L.fo_set_consumer_blocks.restype = [i32], ctypes.c_int
+    L.fo_get_consumer_blocks.argtypes, L.fo_get_consumer_blocks.restype = [], i32
     L.fo_set_poll_timeout_us.argtypes = [i64]
     L.fo_get_poll_timeout_us.restype = i64
     L.fo_device_num_cus.argtypes = [i32, pi32]
@@ -314,6 +317,16 @@ def get_sync_mode():
     p, c = ctypes.c_int32(), ctypes.c_int32()
     lib().fo_get_sync_mode(ctypes.byref(p), ctypes.byref(c))
     return int(p.value), int(c.value)
+
+
+def set_consumer_blocks(max_blocks: int) -> None:
+    """Cap the grid of every consumer launch at `max_blocks` 256-thread
+    workgroups (1 .. 256; process-wide)."""
+    _check(lib().fo_set_consumer_blocks(int(max_blocks)))
+
+
+def get_consumer_blocks() -> int:
+    return int(lib().fo_get_consumer_blocks())
 
 
 def set_poll_timeout_us(us: int) -> None:

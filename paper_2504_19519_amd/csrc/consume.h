@@ -6,12 +6,32 @@
 
 namespace fo {
 
-// Largest consumer grid. With 256-thread workgroups this is at most one
-// wave per SIMD on average, far from what could keep the GEMM off a CU.
+// Largest consumer grid: one 256-thread workgroup (one wave per SIMD) per
+// compute unit at most.
 constexpr int kMaxConsumeBlocks = 256;
+// Segments one launch can carry (a group has R or B of them).
+constexpr int kMaxConsumeSegments = 16;
 
-hipError_t launch_consume(int dtype, int sync, const uint16_t* src, const uint16_t* peer, uint16_t* dst,
-                          int64_t len, const uint32_t* counter, uint32_t target, uint32_t* status,
-                          uint64_t timeout_ticks, hipStream_t s);
+// One contiguous piece of a group: `len` elements at src + src_off (and
+// peer + src_off) go to dst + dst_off.
+struct ConsumeSegment {
+    int64_t src_off, dst_off, len;
+};
+
+struct ConsumeArgs {
+    const uint16_t* src;
+    const uint16_t* peer;        // nullptr: copy
+    uint16_t* dst;
+    const uint32_t* counter;     // nullptr: no wait
+    uint32_t target;
+    uint32_t* status;            // bit 0 set on a timed-out wait (may be nullptr)
+    uint64_t timeout_ticks;      // wall-clock ticks
+    int32_t nseg;                // 1 .. kMaxConsumeSegments
+    ConsumeSegment seg[kMaxConsumeSegments];
+};
+
+// One launch: wait once for *counter >= target, then stream every segment.
+// max_blocks caps the grid (1 .. kMaxConsumeBlocks).
+hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blocks, hipStream_t s);
 
 }  // namespace fo

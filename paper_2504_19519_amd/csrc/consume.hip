@@ -3,20 +3,23 @@
 // until its count reaches the group's tile count; the communication itself
 // is a library call on a contiguous buffer, Section 3.3 Motivation).
 //
-// One launch handles one contiguous segment: every workgroup waits for the
+// One launch handles the contiguous segments of one group (one segment for a
+// plain (ptr, len) call; the R or B destination pieces of a group for the
+// ReduceScatter and All-to-All stand-ins): every workgroup waits for the
 // group's counter (relaxed agent-scope polls with s_sleep; then an
 // agent-scope acquire, or device-coherent loads of the segment, see
-// fo_sync_mode), then streams the segment:
+// fo_sync_mode), then streams each segment with a grid-stride loop:
 //   dst = RNE(src + peer)   AllReduce / ReduceScatter of two partials
 //   dst = src               All-to-All (copy to the receive buffer)
 // The wait is bounded by a wall-clock limit; on timeout the workgroup writes
 // nothing and raises bit 0 of the status word, so a missing signal can never
 // hang the device.
 //
-// The grid is capped (kMaxConsumeBlocks) and a workgroup holds no LDS and few
-// registers, so polling workgroups never take the resources a not yet
-// dispatched GEMM workgroup needs (the GEMM holds 110 KB of LDS, four waves
-// and about half of each SIMD's registers per CU).
+// A consumer workgroup holds 4 bytes of LDS and at most 56 registers per
+// lane, so it fits beside a GEMM workgroup on the same compute unit (the
+// GEMM kernels leave at least 64 registers per SIMD lane and 10 KB of LDS
+// free): polling consumers share compute units with the GEMM instead of
+// taking them away from it.
 #include <hip/hip_runtime.h>
 
 #include "consume.h"
@@ -86,12 +89,11 @@ __device__ __forceinline__ uint16_t add1(uint16_t x, uint16_t y) {
     return (uint16_t)from_f32<DT>(to_f32<DT>(x) + to_f32<DT>(y));
 }
 
-// 16-byte path (FENCE_ALL / FENCE_ONE): src, peer and dst 16-byte aligned.
-template <int DT, bool SUM, int SYNC>
-__global__ __launch_bounds__(kThreads) void consume_vec_kernel(
-    const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer, uint16_t* __restrict__ dst,
-    int64_t len, const uint32_t* counter, uint32_t target, uint32_t* status, uint64_t timeout_ticks) {
-    if (counter && !wait_counter<SYNC>(counter, target, status, timeout_ticks)) return;
+// Stream one segment, 16 bytes per lane per access (FENCE_ALL / FENCE_ONE;
+// src, peer and dst 16-byte aligned): nontemporal loads and stores.
+template <int DT, bool SUM>
+__device__ __forceinline__ void stream_vec16(const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer,
+                                             uint16_t* __restrict__ dst, int64_t len) {
     const int64_t n16 = len >> 3;
     const u32x4_t* s = reinterpret_cast<const u32x4_t*>(src);
     const u32x4_t* q = reinterpret_cast<const u32x4_t*>(peer);
@@ -123,13 +125,13 @@ __global__ __launch_bounds__(kThreads) void consume_vec_kernel(
     }
 }
 
-// 8-byte path with device-coherent source loads (COHERENT): src, peer and
-// dst 8-byte aligned. Two 8-byte units per lane per unrolled step.
+// Stream one segment with device-coherent 8-byte source loads (COHERENT;
+// src, peer and dst 8-byte aligned). Two 8-byte units per lane per
+// unrolled step.
 template <int DT, bool SUM>
-__global__ __launch_bounds__(kThreads) void consume_coherent_kernel(
-    const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer, uint16_t* __restrict__ dst,
-    int64_t len, const uint32_t* counter, uint32_t target, uint32_t* status, uint64_t timeout_ticks) {
-    if (counter && !wait_counter<FO_SYNC_COHERENT>(counter, target, status, timeout_ticks)) return;
+__device__ __forceinline__ void stream_coherent8(const uint16_t* __restrict__ src,
+                                                 const uint16_t* __restrict__ peer,
+                                                 uint16_t* __restrict__ dst, int64_t len) {
     constexpr int U = 2 * kUnroll;
     const int64_t n8 = len >> 2;
     const uint64_t* s = reinterpret_cast<const uint64_t*>(src);
@@ -171,58 +173,76 @@ __global__ __launch_bounds__(kThreads) void consume_coherent_kernel(
     }
 }
 
-// Element path for unaligned buffers: an acquire before plain loads (the
-// coherent mode falls back to FENCE_ONE here).
+// Stream one segment element by element (unaligned buffers).
 template <int DT, bool SUM>
-__global__ __launch_bounds__(kThreads) void consume_elem_kernel(
-    const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer, uint16_t* __restrict__ dst,
-    int64_t len, const uint32_t* counter, uint32_t target, uint32_t* status, uint64_t timeout_ticks) {
-    if (counter && !wait_counter<FO_SYNC_FENCE_ALL>(counter, target, status, timeout_ticks)) return;
+__device__ __forceinline__ void stream_elem(const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer,
+                                            uint16_t* __restrict__ dst, int64_t len) {
     const int64_t stride = (int64_t)gridDim.x * kThreads;
     for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < len; i += stride)
         dst[i] = SUM ? add1<DT>(src[i], peer[i]) : src[i];
 }
 
+enum { kPathVec16 = 0, kPathCoherent8 = 1, kPathElem = 2 };
+
+// SYNC: how the wait publishes the group to the workgroup (wait_counter).
+// PATH: kPathCoherent8 goes with SYNC == COHERENT; kPathElem (unaligned
+// buffers) waits with FENCE_ALL in every mode, since plain loads follow.
+template <int DT, bool SUM, int SYNC, int PATH>
+__global__ __launch_bounds__(kThreads) void consume_kernel(const ConsumeArgs a) {
+    if (a.counter && !wait_counter<SYNC>(a.counter, a.target, a.status, a.timeout_ticks)) return;
+    for (int k = 0; k < a.nseg; ++k) {
+        const ConsumeSegment g = a.seg[k];
+        const uint16_t* src = a.src + g.src_off;
+        const uint16_t* peer = SUM ? a.peer + g.src_off : nullptr;
+        uint16_t* dst = a.dst + g.dst_off;
+        if constexpr (PATH == kPathVec16) stream_vec16<DT, SUM>(src, peer, dst, g.len);
+        else if constexpr (PATH == kPathCoherent8) stream_coherent8<DT, SUM>(src, peer, dst, g.len);
+        else stream_elem<DT, SUM>(src, peer, dst, g.len);
+    }
+}
+
 template <int DT, bool SUM>
-void launch_variant(int sync, bool vec16, bool vec8, dim3 g, dim3 b, hipStream_t s, const uint16_t* src,
-                    const uint16_t* peer, uint16_t* dst, int64_t len, const uint32_t* counter,
-                    uint32_t target, uint32_t* status, uint64_t ticks) {
-    if (sync == FO_SYNC_COHERENT && vec8)
-        hipLaunchKernelGGL((consume_coherent_kernel<DT, SUM>), g, b, 0, s, src, peer, dst, len, counter,
-                           target, status, ticks);
-    else if (sync == FO_SYNC_FENCE_ALL && vec16)
-        hipLaunchKernelGGL((consume_vec_kernel<DT, SUM, FO_SYNC_FENCE_ALL>), g, b, 0, s, src, peer, dst,
-                           len, counter, target, status, ticks);
-    else if (vec16)
-        hipLaunchKernelGGL((consume_vec_kernel<DT, SUM, FO_SYNC_FENCE_ONE>), g, b, 0, s, src, peer, dst,
-                           len, counter, target, status, ticks);
+void launch_variant(int sync, int path, dim3 g, dim3 b, hipStream_t s, const ConsumeArgs& a) {
+    if (path == kPathCoherent8)
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent8>), g, b, 0, s, a);
+    else if (path == kPathVec16 && sync == FO_SYNC_FENCE_ALL)
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ALL, kPathVec16>), g, b, 0, s, a);
+    else if (path == kPathVec16)
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ONE, kPathVec16>), g, b, 0, s, a);
     else
-        hipLaunchKernelGGL((consume_elem_kernel<DT, SUM>), g, b, 0, s, src, peer, dst, len, counter,
-                           target, status, ticks);
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ALL, kPathElem>), g, b, 0, s, a);
 }
 
 }  // namespace
 
-hipError_t launch_consume(int dtype, int sync, const uint16_t* src, const uint16_t* peer, uint16_t* dst,
-                          int64_t len, const uint32_t* counter, uint32_t target, uint32_t* status,
-                          uint64_t timeout_ticks, hipStream_t s) {
-    const uintptr_t bits = reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst) |
-                           reinterpret_cast<uintptr_t>(peer);
+hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blocks, hipStream_t s) {
+    // The path is chosen once for the launch: every segment's pointers must
+    // allow it.
+    uintptr_t bits = 0;
+    int64_t total = 0;
+    for (int k = 0; k < a.nseg; ++k) {
+        bits |= reinterpret_cast<uintptr_t>(a.src + a.seg[k].src_off) |
+                reinterpret_cast<uintptr_t>(a.dst + a.seg[k].dst_off);
+        if (a.peer) bits |= reinterpret_cast<uintptr_t>(a.peer + a.seg[k].src_off);
+        total += a.seg[k].len;
+    }
     const bool vec16 = (bits & 15) == 0, vec8 = (bits & 7) == 0;
-    const bool coherent = sync == FO_SYNC_COHERENT && vec8;
-    const int64_t per_block = coherent ? (int64_t)kThreads * 2 * kUnroll * 4
-                                       : vec16 ? (int64_t)kThreads * kUnroll * 8 : (int64_t)kThreads;
-    int64_t blocks = (len + per_block - 1) / per_block;
+    const int path = sync == FO_SYNC_COHERENT ? (vec8 ? kPathCoherent8 : kPathElem)
+                                              : (vec16 ? kPathVec16 : kPathElem);
+    const int64_t per_block = path == kPathCoherent8 ? (int64_t)kThreads * 2 * kUnroll * 4
+                              : path == kPathVec16   ? (int64_t)kThreads * kUnroll * 8
+                                                     : (int64_t)kThreads;
+    int64_t blocks = (total + per_block - 1) / per_block;
     if (blocks < 1) blocks = 1;
-    if (blocks > kMaxConsumeBlocks) blocks = kMaxConsumeBlocks;
+    if (blocks > max_blocks) blocks = max_blocks;
     const dim3 g((unsigned)blocks), b(kThreads);
-    const bool sum = peer != nullptr;
+    const bool sum = a.peer != nullptr;
     if (dtype == FO_FP16) {
-        if (sum) launch_variant<FO_FP16, true>(sync, vec16, vec8, g, b, s, src, peer, dst, len, counter, target, status, timeout_ticks);
-        else launch_variant<FO_FP16, false>(sync, vec16, vec8, g, b, s, src, peer, dst, len, counter, target, status, timeout_ticks);
+        if (sum) launch_variant<FO_FP16, true>(sync, path, g, b, s, a);
+        else launch_variant<FO_FP16, false>(sync, path, g, b, s, a);
     } else {
-        if (sum) launch_variant<FO_BF16, true>(sync, vec16, vec8, g, b, s, src, peer, dst, len, counter, target, status, timeout_ticks);
-        else launch_variant<FO_BF16, false>(sync, vec16, vec8, g, b, s, src, peer, dst, len, counter, target, status, timeout_ticks);
+        if (sum) launch_variant<FO_BF16, true>(sync, path, g, b, s, a);
+        else launch_variant<FO_BF16, false>(sync, path, g, b, s, a);
     }
     return hipGetLastError();
 }

@@ -7,14 +7,17 @@
 // in the reordered output (Section 3.3 Approach (1)).
 //
 // Main loop: MFMA v_mfma_f32_32x32x16 (fp16 / bf16 in, fp32 accumulate) on
-// k steps of 64. A and W tiles move from HBM straight into a 3-stage LDS ring
-// (direct global-to-LDS loads, XOR-swizzled rows for conflict-free 16-byte
-// fragment reads), issued three steps ahead; fragments of the next 16-wide
-// k step are read while the MFMAs of the current one run. The main loop is
-// the same for every output pattern (Section 5: only the epilogue changes).
+// k steps of 64, four waves in a 2 x 2 arrangement. A and W tiles move from
+// memory straight into an LDS ring of STAGES stages (direct global-to-LDS
+// loads, XOR-swizzled rows for conflict-free 16-byte fragment reads), issued
+// STAGES steps ahead; fragments of the next 16-wide k step are read while the
+// MFMAs of the current one run, and every LDS read and load issue sits in the
+// shadow of an MFMA. The main loop is the same for every output pattern
+// (Section 5: only the epilogue changes).
 //
 // Epilogue (Section 3.3 Approach; Section 3.2 Approach):
-//   1. accumulators -> fp16/bf16 (round to nearest even) -> LDS staging tile;
+//   1. accumulators -> fp16/bf16 (round to nearest even) -> LDS staging tile
+//      (in two passes of half the rows when the tile does not fit);
 //   2. every tile row goes out as full-row stores to its destination:
 //      row-major C, the tile's slot (tile pattern), the slice's place in its
 //      group segment (subtile pattern) or the row's pool position (subtoken
@@ -31,9 +34,7 @@
 namespace fo {
 namespace {
 
-constexpr int kThreads = 256;
 constexpr int kBK = 64;             // k values per main-loop step (128 bytes of fp16)
-constexpr int kStages = 3;          // LDS ring depth: loads run two steps ahead
 // s_waitcnt operand for vmcnt = vm and lgkmcnt = lgkm, expcnt at its maximum
 // (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[5:4] at 15:14)
 constexpr int wait_imm(int vm, int lgkm) {
@@ -60,23 +61,27 @@ __device__ __forceinline__ f32x16_t mfma32(u32x4_t a, u32x4_t b, f32x16_t c) {
 // share a 256-byte bank line, so the 16 rows read together at one k position
 // must land in 16 different (row parity, slot) pairs, which this swizzle
 // gives for any 16 consecutive rows.
-template <int BM, int BN>
+template <int BM, int BN, int STAGES, int NW>
 struct Tiles {
     static constexpr int kRow = kBK * 2;
     static constexpr int kA = BM * kRow, kB = BN * kRow;
     static constexpr int kStage = kA + kB;
     static constexpr int kLDC = BN + 8;                  // staging row (halfs)
-    static constexpr int kStaging = BM * kLDC * 2;
-    static constexpr int kAI = kA / 1024 / 4;            // 1 KB load blocks per wave
-    static constexpr int kBI = kB / 1024 / 4;
+    // rows staged at once: the whole tile, or half of it, in two stages
+    static constexpr int kRowsPerPass = BM * kLDC * 2 <= 2 * kStage ? BM : BM / 2;
+    static constexpr int kPasses = BM / kRowsPerPass;
+    static constexpr int kAI = kA / 1024 / NW;           // 1 KB load blocks per wave
+    static constexpr int kBI = kB / 1024 / NW;
+    static constexpr int kLoads = kAI + kBI;
 };
 
-// Start loading one k step of this workgroup's A rows (into the first kA
+// Start loading one k step of this workgroup's A rows (into the first KA
 // bytes of `st`) and W rows (after them) with direct global-to-LDS loads:
 // each instruction moves 64 x 16 bytes into one 1 KB block. The rows are
 // addressed through buffer resources over the tile's row blocks (a_bytes and
-// w_bytes long; the host checks they fit in 32 bits), so a read past them
-// returns zero instead of faulting.
+// w_bytes long; the host checks they fit in 32 bits): a read past them
+// returns zero instead of faulting, and a resource of length 0 loads zeros
+// without touching memory.
 template <int AI, int BI, int KA>
 __device__ __forceinline__ void issue_tile(const uint16_t* Ablk, const uint16_t* Wblk, uint32_t a_bytes,
                                            uint32_t w_bytes, const uint32_t* voffA, const uint32_t* voffB,
@@ -96,18 +101,18 @@ __device__ __forceinline__ void issue_tile(const uint16_t* Ablk, const uint16_t*
 }
 
 // Instruction order inside one k-step phase of the main loop: each MFMA
-// (32 cycles of matrix work) carries one LDS fragment read and, in the last
-// phase, up to DPM direct-to-LDS load issues in its shadow, so the matrix
-// pipe does not drain while reads and loads are issued.
-template <int MFMA, int READS, int DMA, int DPM>
+// (32 cycles of matrix work) carries up to R LDS fragment reads and V
+// direct-to-LDS load issues in its shadow, so the matrix pipe does not
+// drain while they are issued.
+template <int MFMA, int R, int V>
 __device__ __forceinline__ void interleave_phase() {
+    constexpr int r1 = (R + MFMA - 1) / MFMA, v1 = (V + MFMA - 1) / MFMA;
 #pragma unroll
     for (int i = 0; i < MFMA; ++i) {
-        if (i < READS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);          // LDS read
-        if (DPM > 0 && i * DPM < DMA) __builtin_amdgcn_sched_group_barrier(0x020, DPM, 0);  // VMEM
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                         // MFMA
+        if (i * r1 < R) __builtin_amdgcn_sched_group_barrier(0x100, r1, 0);   // LDS read
+        if (i * v1 < V) __builtin_amdgcn_sched_group_barrier(0x020, v1, 0);   // global load
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                    // MFMA
     }
-    if (READS > MFMA) __builtin_amdgcn_sched_group_barrier(0x100, READS - MFMA, 0);
 }
 
 // One main-loop synchronization: this wave waits until at most `vm` of its
@@ -126,22 +131,26 @@ __device__ __forceinline__ void wait_and_barrier() {
     asm volatile("" ::: "memory");
 }
 
-template <int DT, int BM, int BN, int WAVES_M, int WAVES_N>
-__global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs a) {
+template <int DT, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(const GemmArgs a) {
+    constexpr int NW = WAVES_M * WAVES_N, NT = 64 * NW;
     constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
     constexpr int MI = WTM / 32, NJ = WTN / 32;
-    using T = Tiles<BM, BN>;
-    static_assert(WAVES_M * WAVES_N == kThreads / 64, "four waves");
+    using T = Tiles<BM, BN, STAGES, NW>;
+    static_assert(NW == 4 || NW == 8, "four or eight waves");
+    static_assert(NT >= BM, "one thread per tile row in the epilogue set-up");
     static_assert(WTM % 32 == 0 && WTN % 32 == 0, "32x32 MFMA blocks");
-    static_assert(T::kAI >= 1 && T::kBI >= 1 && T::kA % 4096 == 0 && T::kB % 4096 == 0,
+    static_assert(STAGES == 2 || STAGES == 3, "two or three LDS stages");
+    static_assert(T::kAI >= 1 && T::kBI >= 1 && T::kA % (1024 * NW) == 0 && T::kB % (1024 * NW) == 0,
                   "each wave loads whole 1 KB blocks");
-    static_assert(T::kStaging <= 2 * T::kStage, "output staging fits in two stages");
+    static_assert(T::kRowsPerPass * T::kLDC * 2 <= 2 * T::kStage, "output staging fits in two stages");
+    static_assert(T::kRowsPerPass % WTM == 0, "a staging pass holds whole wave rows");
 
-    // Three stages in separate arrays, so that the compiler can tell the
+    // The stages live in separate arrays, so that the compiler can tell the
     // stage being read from the stages being filled.
     __shared__ __attribute__((aligned(1024))) char st0[T::kStage];
     __shared__ __attribute__((aligned(1024))) char st1[T::kStage];
-    __shared__ __attribute__((aligned(1024))) char st2[T::kStage];
+    __shared__ __attribute__((aligned(1024))) char st2[STAGES == 3 ? T::kStage : 1024];
     __shared__ int64_t row_off[BM];
 
     const int tid = threadIdx.x;
@@ -223,55 +232,57 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
                 acc[i][j] = mfma32<DT>(fb[j], fa[i], acc[i][j]);
     };
 
+    constexpr int kMfma = MI * NJ, kReads = MI + NJ;
     // Step kt multiplies the tile in stage `cur` (its k step 0 fragments are
-    // already in fa0/fb0). Before its last k step, every wave has read all of
-    // `cur` and tile kt+1 has landed: after the barrier, tile kt+3 goes into
-    // `cur` and the first fragments of tile kt+1 (stage `nxt`) are read while
-    // the last MFMAs of tile kt run.
-    constexpr int kMfma = MI * NJ, kReads = MI + NJ, kDma = T::kAI + T::kBI;
-    constexpr int kDmaPerMfma = (kDma + kMfma - 1) / kMfma;
-
-    // Step kt multiplies the tile in stage `cur` (its k step 0 fragments are
-    // already in fa0/fb0). Before its last k step, every wave has read all of
-    // `cur` and tile kt+1 has landed: after the barrier, tile kt+3 goes into
-    // `cur` and the first fragments of tile kt+1 (stage `nxt`) are read while
-    // the last MFMAs of tile kt run.
+    // already in fa0/fb0; tile kt+1 is in stage `nxt`). Before its last k
+    // step, every wave has read all of `cur` and tile kt+1 has landed (tiles
+    // up to kt+STAGES-1 may still be loading): after the barrier, tile
+    // kt+STAGES goes into `cur`, and the first fragments of tile kt+1 are read
+    // while the last MFMAs of tile kt run.
     auto step = [&](int kt, char* cur, const char* nxt) {
         load_frags(cur, 1, fa1, fb1);
         mma(fa0, fb0);
-        interleave_phase<kMfma, kReads, 0, 0>();
+        interleave_phase<kMfma, kReads, 0>();
         __builtin_amdgcn_sched_barrier(0);
         load_frags(cur, 2, fa0, fb0);
         mma(fa1, fb1);
-        interleave_phase<kMfma, kReads, 0, 0>();
+        interleave_phase<kMfma, kReads, 0>();
         __builtin_amdgcn_sched_barrier(0);
         load_frags(cur, 3, fa1, fb1);
         mma(fa0, fb0);
-        interleave_phase<kMfma, kReads, 0, 0>();
+        interleave_phase<kMfma, kReads, 0>();
         __builtin_amdgcn_sched_barrier(0);
-        wait_and_barrier<T::kAI + T::kBI>();
-        issue(kt + 3, cur);
+        wait_and_barrier<(STAGES - 2) * T::kLoads>();
+        issue(kt + STAGES, cur);
         load_frags(nxt, 0, fa0, fb0);
         mma(fa1, fb1);
-        interleave_phase<kMfma, kReads, kDma, kDmaPerMfma>();
+        interleave_phase<kMfma, kReads, T::kLoads>();
         __builtin_amdgcn_sched_barrier(0);
     };
 
     issue(0, st0);
     issue(1, st1);
-    issue(2, st2);
-    wait_and_barrier<2 * (T::kAI + T::kBI)>();
+    if constexpr (STAGES == 3) issue(2, st2);
+    wait_and_barrier<(STAGES - 1) * T::kLoads>();
     load_frags(st0, 0, fa0, fb0);
     int kt = 0;
-    for (; kt + 3 <= KT; kt += 3) {      // tile t lives in stage t % 3
-        step(kt, st0, st1);
-        step(kt + 1, st1, st2);
-        step(kt + 2, st2, st0);
+    if constexpr (STAGES == 3) {
+        for (; kt + 3 <= KT; kt += 3) {      // tile t lives in stage t % 3
+            step(kt, st0, st1);
+            step(kt + 1, st1, st2);
+            step(kt + 2, st2, st0);
+        }
+        if (kt < KT) step(kt, st0, st1);
+        if (kt + 1 < KT) step(kt + 1, st1, st2);
+    } else {
+        for (; kt + 2 <= KT; kt += 2) {      // tile t lives in stage t % 2
+            step(kt, st0, st1);
+            step(kt + 1, st1, st0);
+        }
+        if (kt < KT) step(kt, st0, st1);
     }
-    if (kt < KT) step(kt, st0, st1);
-    if (kt + 1 < KT) step(kt + 1, st1, st2);
     wait_and_barrier<0>();    // no load may still be writing LDS
-    __syncthreads();     // operand stages are reused for the output tile
+    __syncthreads();          // operand stages are reused for the output tile
 
     // ---- epilogue -------------------------------------------------------
     // Destination of row `tid` of the tile, by pattern.
@@ -296,81 +307,95 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_signal_kernel(const GemmArgs
         row_off[r] = off;
     }
 
-    // accumulators -> LDS staging [BM][BN + 8], rows [0, BM/2) in stage 0
-    // and [BM/2, BM) in stage 1 (the loop ended with a barrier)
+    // Staging row r of a pass ([0, kRowsPerPass)): the first half of the
+    // rows in stage 0, the second half in stage 1.
+    constexpr int kHalf = T::kRowsPerPass / 2;
     auto crow = [&](int r) -> uint16_t* {
-        return reinterpret_cast<uint16_t*>(r < BM / 2 ? st0 + r * T::kLDC * 2 : st1 + (r - BM / 2) * T::kLDC * 2);
+        return reinterpret_cast<uint16_t*>(r < kHalf ? st0 + r * T::kLDC * 2 : st1 + (r - kHalf) * T::kLDC * 2);
     };
+    const bool coherent = a.counters && a.sync == FO_SYNC_COHERENT;
 #pragma unroll
-    for (int i = 0; i < MI; ++i) {
-        const int m = wm * WTM + i * 32 + (lane & 31);
+    for (int pass = 0; pass < T::kPasses; ++pass) {
+        const int r0 = pass * T::kRowsPerPass;
+        // accumulators of the waves whose rows are in this pass -> staging
+        if (wm * WTM >= r0 && wm * WTM < r0 + T::kRowsPerPass) {
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
+            for (int i = 0; i < MI; ++i) {
+                const int m = wm * WTM - r0 + i * 32 + (lane & 31);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int n = wn * WTN + j * 32 + q * 8 + (lane >> 5) * 4;
-                u32x2_t v;
-                v[0] = pack2<DT>(acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]);
-                v[1] = pack2<DT>(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-                *reinterpret_cast<u32x2_t*>(crow(m) + n) = v;
+                for (int j = 0; j < NJ; ++j) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int n = wn * WTN + j * 32 + q * 8 + (lane >> 5) * 4;
+                        u32x2_t v;
+                        v[0] = pack2<DT>(acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]);
+                        v[1] = pack2<DT>(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+                        *reinterpret_cast<u32x2_t*>(crow(m) + n) = v;
+                    }
+                }
             }
         }
-    }
-    __syncthreads();
-
-    if (a.counters && a.sync == FO_SYNC_COHERENT) {
-        // Device-coherent 8-byte stores (written through to the point all
-        // chiplets share), each wave waits until its stores are complete,
-        // then one lane counts the tile: no cache write-back is needed.
-        constexpr int LPR = BN / 4;             // lanes per row (8 bytes each)
-        constexpr int RPI = 64 / LPR;           // rows per wave instruction
-        const int lr = lane / LPR, lc = lane % LPR;
+        __syncthreads();
+        if (coherent) {
+            // Device-coherent 8-byte stores (written through to the point all
+            // chiplets share): no cache write-back is needed before the signal.
+            constexpr int LPR = BN / 4;             // lanes per row (8 bytes each)
+            constexpr int RPI = LPR >= 64 ? 1 : 64 / LPR;   // rows per wave instruction
+            constexpr int CPL = LPR >= 64 ? LPR / 64 : 1;   // 8-byte columns per lane
+            const int lr = LPR >= 64 ? 0 : lane / LPR;
+            const int lc = LPR >= 64 ? lane : lane % LPR;
 #pragma unroll 4
-        for (int r = wave * RPI + lr; r < BM; r += 4 * RPI) {
-            const uint64_t v = *reinterpret_cast<const uint64_t*>(crow(r) + lc * 4);
-            __hip_atomic_store(reinterpret_cast<uint64_t*>(a.C + row_off[r]) + lc, v, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
+            for (int r = wave * RPI + lr; r < T::kRowsPerPass; r += NW * RPI) {
+#pragma unroll
+                for (int cc = 0; cc < CPL; ++cc) {
+                    const int col = lc + cc * 64;
+                    const uint64_t v = *reinterpret_cast<const uint64_t*>(crow(r) + col * 4);
+                    __hip_atomic_store(reinterpret_cast<uint64_t*>(a.C + row_off[r0 + r]) + col, v,
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+        } else {
+            constexpr int CPR = BN / 8;             // 16-byte chunks per tile row
+            constexpr int RPP = NT / CPR;           // rows per pass of the workgroup
+            const int c = tid % CPR;
+#pragma unroll 4
+            for (int r = tid / CPR; r < T::kRowsPerPass; r += RPP) {
+                const u32x4_t v = *reinterpret_cast<const u32x4_t*>(crow(r) + c * 8);
+                *reinterpret_cast<u32x4_t*>(a.C + row_off[r0 + r] + c * 8) = v;
+            }
         }
+        if (pass + 1 < T::kPasses) __syncthreads();   // staging is refilled
+    }
+
+    if (!a.counters) return;
+    // Section 3.2: count the finished tile for its group once all of the
+    // tile's stores are visible to every compute unit.
+    if (coherent) {
+        // each wave waits until its write-through stores are complete
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         __syncthreads();
         if (tid == 0)
             __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELAXED,
                                    __HIP_MEMORY_SCOPE_AGENT);
-        return;
-    }
-
-    constexpr int CPR = BN / 8;                 // 16-byte chunks per tile row
-    constexpr int RPP = kThreads / CPR;         // rows per pass
-    const int c = tid % CPR;
-#pragma unroll 4
-    for (int r = tid / CPR; r < BM; r += RPP) {
-        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(crow(r) + c * 8);
-        *reinterpret_cast<u32x4_t*>(a.C + row_off[r] + c * 8) = v;
-    }
-
-    if (a.counters) {
-        // Section 3.2: count the finished tile for its group once all of the
-        // tile's stores are visible to every compute unit.
-        if (a.sync == FO_SYNC_FENCE_ALL) {
-            // every wave: release fence at agent scope (L2 write-back + wait)
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-            __syncthreads();
-            if (tid == 0)
-                __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
-        } else {
-            // workgroup barrier, then one release increment (one write-back)
-            __syncthreads();
-            if (tid == 0)
-                __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELEASE,
-                                       __HIP_MEMORY_SCOPE_AGENT);
-        }
+    } else if (a.sync == FO_SYNC_FENCE_ALL) {
+        // every wave: release fence at agent scope (L2 write-back + wait)
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        __syncthreads();
+        if (tid == 0)
+            __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+        // workgroup barrier, then one release increment (one write-back)
+        __syncthreads();
+        if (tid == 0)
+            __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELEASE,
+                                   __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
-template <int DT, int BM, int BN, int WM, int WN>
+template <int DT, int BM, int BN, int WM, int WN, int ST>
 hipError_t launch_t(const GemmArgs& a, int grid, hipStream_t s) {
-    hipLaunchKernelGGL((gemm_signal_kernel<DT, BM, BN, WM, WN>), dim3(grid), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((gemm_signal_kernel<DT, BM, BN, WM, WN, ST>), dim3(grid), dim3(64 * WM * WN), 0, s, a);
     return hipGetLastError();
 }
 
@@ -378,16 +403,20 @@ hipError_t launch_t(const GemmArgs& a, int grid, hipStream_t s) {
 
 hipError_t launch_gemm(int dtype, int tile_m, int tile_n, const GemmArgs& a, int grid, hipStream_t s) {
     if (tile_m == 256 && tile_n == 128)
-        return dtype == FO_FP16 ? launch_t<FO_FP16, 256, 128, 2, 2>(a, grid, s)
-                                : launch_t<FO_BF16, 256, 128, 2, 2>(a, grid, s);
+        return dtype == FO_FP16 ? launch_t<FO_FP16, 256, 128, 2, 2, 3>(a, grid, s)
+                                : launch_t<FO_BF16, 256, 128, 2, 2, 3>(a, grid, s);
+    if (tile_m == 256 && tile_n == 256)
+        return dtype == FO_FP16 ? launch_t<FO_FP16, 256, 256, 2, 4, 2>(a, grid, s)
+                                : launch_t<FO_BF16, 256, 256, 2, 4, 2>(a, grid, s);
     if (tile_m == 64 && tile_n == 64)
-        return dtype == FO_FP16 ? launch_t<FO_FP16, 64, 64, 2, 2>(a, grid, s)
-                                : launch_t<FO_BF16, 64, 64, 2, 2>(a, grid, s);
+        return dtype == FO_FP16 ? launch_t<FO_FP16, 64, 64, 2, 2, 3>(a, grid, s)
+                                : launch_t<FO_BF16, 64, 64, 2, 2, 3>(a, grid, s);
     return hipErrorInvalidValue;
 }
 
 bool gemm_tile_supported(int tile_m, int tile_n) {
-    return (tile_m == 256 && tile_n == 128) || (tile_m == 64 && tile_n == 64);
+    return (tile_m == 256 && tile_n == 128) || (tile_m == 256 && tile_n == 256) ||
+           (tile_m == 64 && tile_n == 64);
 }
 
 }  // namespace fo

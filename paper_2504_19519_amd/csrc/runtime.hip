@@ -2,7 +2,9 @@
 // kernel launches and the two-stream orchestration of one overlapped run.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
+#include <cstdint>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
@@ -34,6 +36,15 @@ int env_mode(const char* name, int dflt) {
 }
 std::atomic<int> g_sync_producer{env_mode("FO_SYNC_PRODUCER", FO_SYNC_COHERENT)};
 std::atomic<int> g_sync_consumer{env_mode("FO_SYNC_CONSUMER", FO_SYNC_COHERENT)};
+std::atomic<int> g_consumer_blocks{[] {
+    const char* e = std::getenv("FO_CONSUMER_BLOCKS");
+    if (e && *e) {
+        char* end = nullptr;
+        const long v = std::strtol(e, &end, 10);
+        if (end && *end == '\0' && v >= 1 && v <= kMaxConsumeBlocks) return (int)v;
+    }
+    return kMaxConsumeBlocks;
+}()};
 
 constexpr int kMaxDevices = 64;
 std::atomic<int64_t> g_clock_khz[kMaxDevices];   // 0 = unknown
@@ -72,6 +83,22 @@ const T* dev_table(const void* dev_plan, int64_t word_off) {
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+// Common fields of a consumer launch; the wait limit in device clock ticks.
+fo_status consume_args(const uint16_t* src, const uint16_t* peer, uint16_t* dst, const uint32_t* counter,
+                       uint32_t target, uint32_t* status, ConsumeArgs* a) {
+    int64_t khz = 0;
+    fo_status st = clock_khz(&khz);
+    if (st != FO_OK) return st;
+    a->src = src;
+    a->peer = peer;
+    a->dst = dst;
+    a->counter = counter;
+    a->target = target;
+    a->status = status;
+    a->timeout_ticks = (uint64_t)poll_timeout_us() * (uint64_t)khz / 1000u;
+    return FO_OK;
+}
 
 }  // namespace
 
@@ -120,6 +147,16 @@ void fo_get_sync_mode(int32_t* producer, int32_t* consumer) {
     if (consumer) *consumer = fo::g_sync_consumer.load();
 }
 
+fo_status fo_set_consumer_blocks(int32_t max_blocks) {
+    fo::clear_error();
+    if (max_blocks < 1 || max_blocks > fo::kMaxConsumeBlocks)
+        return fo::fail(FO_ERR_ARG, "max_blocks must be in [1, 256]");
+    fo::g_consumer_blocks.store(max_blocks);
+    return FO_OK;
+}
+
+int32_t fo_get_consumer_blocks(void) { return fo::g_consumer_blocks.load(); }
+
 fo_status fo_device_num_cus(int32_t device, int32_t* num_cus) {
     fo::clear_error();
     if (!num_cus) return fo::fail(FO_ERR_ARG, "num_cus is NULL");
@@ -149,8 +186,11 @@ fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan, cons
     if (!dev_plan && (plan->pattern != FO_PATTERN_ROWMAJOR || counters))
         return fo::fail(FO_ERR_ARG, "dev_plan is NULL");
     if (!fo::gemm_tile_supported(plan->tile_m, plan->tile_n))
-        return fo::fail(FO_ERR_UNSUPPORTED, "GEMM kernels exist for 256x128 and 64x64 tiles");
+        return fo::fail(FO_ERR_UNSUPPORTED, "GEMM kernels exist for 256x128, 256x256 and 64x64 tiles");
     if (plan->K % 64) return fo::fail(FO_ERR_SHAPE, "K must be a multiple of 64");
+    // operand row blocks are addressed with 32-bit byte offsets
+    if ((int64_t)std::max(plan->tile_m, plan->tile_n) * plan->K * 2 > INT32_MAX)
+        return fo::fail(FO_ERR_SHAPE, "tile rows x K x 2 bytes must fit in 31 bits");
     if (!fo::aligned16(A) || !fo::aligned16(W) || !fo::aligned16(C_out))
         return fo::fail(FO_ERR_ARG, "A, W and C_out must be 16-byte aligned");
     if (dev_plan && !fo::aligned16(dev_plan)) return fo::fail(FO_ERR_ARG, "dev_plan must be 16-byte aligned");
@@ -187,14 +227,14 @@ fo_status fo_consume_group(const void* src, const void* peer, void* dst, int64_t
     if (dtype != FO_FP16 && dtype != FO_BF16) return fo::fail(FO_ERR_ARG, "bad dtype");
     if (len == 0 && !counter) return FO_OK;
     if (len > 0 && (!src || !dst)) return fo::fail(FO_ERR_ARG, "null src or dst");
-    int64_t khz = 0;
-    fo_status st = fo::clock_khz(&khz);
+    fo::ConsumeArgs a{};
+    fo_status st = fo::consume_args(static_cast<const uint16_t*>(src), static_cast<const uint16_t*>(peer),
+                                    static_cast<uint16_t*>(dst), counter, target, status_word, &a);
     if (st != FO_OK) return st;
-    const uint64_t ticks = (uint64_t)fo::poll_timeout_us() * (uint64_t)khz / 1000u;
-    hipError_t e = fo::launch_consume(dtype, fo::g_sync_consumer.load(std::memory_order_relaxed),
-                                      static_cast<const uint16_t*>(src),
-                                      static_cast<const uint16_t*>(peer), static_cast<uint16_t*>(dst),
-                                      len, counter, target, status_word, ticks, (hipStream_t)stream);
+    a.nseg = 1;
+    a.seg[0] = fo::ConsumeSegment{0, 0, len};
+    hipError_t e = fo::launch_consume(dtype, fo::g_sync_consumer.load(std::memory_order_relaxed), a,
+                                      fo::g_consumer_blocks.load(std::memory_order_relaxed), (hipStream_t)stream);
     return e == hipSuccess ? FO_OK : fo::hip_fail("consumer launch", e);
 }
 
@@ -296,18 +336,29 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
         return st;
     if (gemm_end_event && (e = hipEventRecord((hipEvent_t)gemm_end_event, s1)) != hipSuccess)
         return fo::hip_fail("hipEventRecord", e);
+    // One consumer launch per group (more if a group has more pieces than a
+    // launch carries), as a collective library would take one call per
+    // group. Groups before the last one share the device with the GEMM and
+    // use the configured grid cap; the last group runs once the GEMM is
+    // done and takes the full grid.
     const int64_t* seg = plan->segs.data();
     const int nseg = (int)(plan->segs.size() / 5);
-    const uint16_t* src16 = static_cast<const uint16_t*>(C_out);
-    const uint16_t* peer16 = static_cast<const uint16_t*>(peer);
-    uint16_t* dst16 = static_cast<uint16_t*>(dst);
-    for (int i = 0; i < nseg; ++i) {
-        const int64_t j = seg[5 * i], so = seg[5 * i + 2], dof = seg[5 * i + 3], len = seg[5 * i + 4];
-        if (len == 0) continue;
-        st = fo_consume_group(src16 + so, peer16 ? peer16 + so : nullptr, dst16 + dof, len, plan->dtype,
-                              overlap ? counters + j : nullptr, (uint32_t)plan->targets[j], status_word,
-                              overlap ? s2 : s1);
-        if (st != FO_OK) return st;
+    const int sync = fo::g_sync_consumer.load(std::memory_order_relaxed);
+    const int cap = fo::g_consumer_blocks.load(std::memory_order_relaxed);
+    fo::ConsumeArgs a{};
+    for (int i = 0; i < nseg;) {
+        const int64_t j = seg[5 * i];
+        if ((st = fo::consume_args(static_cast<const uint16_t*>(C_out), static_cast<const uint16_t*>(peer),
+                                   static_cast<uint16_t*>(dst), overlap ? counters + j : nullptr,
+                                   (uint32_t)plan->targets[j], status_word, &a)) != FO_OK)
+            return st;
+        a.nseg = 0;
+        for (; i < nseg && seg[5 * i] == j && a.nseg < fo::kMaxConsumeSegments; ++i)
+            if (seg[5 * i + 4] > 0) a.seg[a.nseg++] = fo::ConsumeSegment{seg[5 * i + 2], seg[5 * i + 3], seg[5 * i + 4]};
+        if (a.nseg == 0) continue;
+        const int blocks = j + 1 == plan->P ? fo::kMaxConsumeBlocks : cap;
+        if ((e = fo::launch_consume(plan->dtype, sync, a, blocks, overlap ? s2 : s1)) != hipSuccess)
+            return fo::hip_fail("consumer launch", e);
     }
     if (overlap) {
         if ((e = hipEventRecord(e1, s2)) != hipSuccess) return fo::hip_fail("hipEventRecord", e);

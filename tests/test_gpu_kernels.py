@@ -48,6 +48,8 @@ def _gemm(plan, A, W, counters=None, poison=None):
 @pytest.mark.parametrize("dtype", ["fp16", "bf16"])
 @pytest.mark.parametrize("tile,shape", [((256, 128), (512, 384, 320)),
                                         ((256, 128), (1024, 640, 192)),
+                                        ((256, 256), (768, 512, 320)),
+                                        ((256, 256), (512, 768, 3584)),
                                         ((64, 64), (256, 256, 256)),
                                         ((64, 64), (192, 320, 128))])
 def test_plain_gemm_matches_oracle(dtype, tile, shape):
@@ -61,7 +63,7 @@ def test_plain_gemm_matches_oracle(dtype, tile, shape):
 
 
 @pytest.mark.parametrize("K", [64 * kt for kt in range(1, 10)] + [64 * 56])
-@pytest.mark.parametrize("tile", [(256, 128), (64, 64)])
+@pytest.mark.parametrize("tile", [(256, 128), (256, 256), (64, 64)])
 def test_gemm_every_k_step_count(K, tile):
     # the main loop runs k steps in groups of three; cover every remainder
     M, N = 2 * tile[0], 3 * tile[1]
@@ -74,7 +76,7 @@ def test_gemm_every_k_step_count(K, tile):
 
 
 @pytest.mark.parametrize("dtype", ["fp16", "bf16"])
-@pytest.mark.parametrize("tile", [(256, 128), (64, 64)])
+@pytest.mark.parametrize("tile", [(256, 128), (256, 256), (64, 64)])
 def test_identity_operand_is_exact(dtype, tile):
     # A = I: every output is one product by 1 plus sums of zeros, so C = B
     # exactly, whatever the accumulation order (pins the epilogue layout).
@@ -100,20 +102,22 @@ def test_k_zero_gives_zeros():
 @pytest.mark.parametrize("pattern,nd", [("tile", 0), ("subtile", 4), ("subtoken", 8), ("rowmajor", 0)])
 @pytest.mark.parametrize("dtype", ["fp16", "bf16"])
 @pytest.mark.parametrize("sizes", [(1, 2), (3,), (1, 1, 1)])
-def test_reordered_output_is_permuted_plain_output(pattern, nd, dtype, sizes):
-    # 4 x 5 tiles of 256x128 on a modelled 8-CU device: W = 8, T = 3 with a
-    # 4-tile last wave; the XCD order with 8 chiplets on 20 tiles is ragged.
-    M, N, K = 1024, 640, 256
-    say(f"[reorder] pattern={pattern} dtype={dtype} sizes={sizes}")
+@pytest.mark.parametrize("tile", [(256, 128), (256, 256)])
+def test_reordered_output_is_permuted_plain_output(pattern, nd, dtype, sizes, tile):
+    # 4 x 5 tiles on a modelled 8-CU device: W = 8, T = 3 with a 4-tile last
+    # wave; the XCD order with 8 chiplets on 20 tiles is ragged.
+    M, N, K = 4 * tile[0], 5 * tile[1], 256
+    say(f"[reorder] pattern={pattern} dtype={dtype} sizes={sizes} tile={tile}")
     rng = np.random.default_rng(13)
     A, W = _operands(M, N, K, dtype, 14)
     sigma = rng.permutation(nd) if pattern == "subtile" else None
     bucket = rng.integers(0, nd, M) if pattern == "subtoken" else None
-    common = dict(dtype=dtype, order="xcd", num_cus=8, num_dest=nd, dest_perm=sigma, row_bucket=bucket)
+    common = dict(dtype=dtype, tile_m=tile[0], tile_n=tile[1], order="xcd", num_cus=8, num_dest=nd,
+                  dest_perm=sigma, row_bucket=bucket)
     plain = fo.plan_groups(M, N, K, pattern="rowmajor", sizes=list(sizes), **common)
     C = _gemm(plain, A, W, poison=dtype)
     plan = fo.plan_groups(M, N, K, pattern=pattern, sizes=list(sizes), **common)
-    o = oracle.make_plan(M, N, 256, 128, num_cus=8, order="xcd", pattern=pattern, num_dest=nd,
+    o = oracle.make_plan(M, N, tile[0], tile[1], num_cus=8, order="xcd", pattern=pattern, num_dest=nd,
                          sigma=sigma, bucket=bucket, sizes=sizes)
     counters = zeros_u32(plan.P)
     Cr = _gemm(plan, A, W, counters=counters, poison=dtype)

@@ -107,8 +107,8 @@ SMALL = {
     # workload: (M, N, K, modelled CUs, partition in waves)
     "tiny": None,
     "ar_2048x4096x4096": (1024, 1024, 512, 8, (1, 2, 1)),
-    "rs_8192x8192x3584": (1024, 1024, 512, 8, (2, 1, 1)),
-    "ar_rmsnorm_16384x4096x3584_bf16": (1024, 1024, 512, 8, (1, 1, 2)),
+    "rs_8192x8192x3584": (1024, 1280, 512, 8, (2, 1)),          # 256x256 tiles: 20 tiles, T = 3
+    "ar_rmsnorm_16384x4096x3584_bf16": (1024, 1280, 512, 8, (1, 2)),
     "a2a_4096x7168x2048": (1024, 896, 512, 8, (1, 1, 2)),
 }
 
@@ -154,8 +154,8 @@ def test_small_workloads(name):
 
 FULL = {
     "ar_2048x4096x4096": [(1,)],
-    "rs_8192x8192x3584": [(1,) * 8, (2, 2, 2, 2)],
-    "ar_rmsnorm_16384x4096x3584_bf16": [(1,) * 8],
+    "rs_8192x8192x3584": [(1,) * 4, (2, 2), (1, 3)],
+    "ar_rmsnorm_16384x4096x3584_bf16": [(1,) * 4],
     "a2a_4096x7168x2048": [(1, 1, 1, 1)],
 }
 
@@ -211,3 +211,21 @@ def test_sync_modes(producer, consumer, name):
         check(w, inp, plan, o)
     finally:
         fo.set_sync_mode(*old)
+
+
+@pytest.mark.parametrize("blocks", [1, 3, 64])
+@pytest.mark.parametrize("name", ["ar_2048x4096x4096", "rs_8192x8192x3584", "a2a_4096x7168x2048"])
+def test_consumer_grid_cap(blocks, name):
+    # a capped consumer grid (grid-stride over every piece of the group)
+    # gives the same bits as the full grid
+    old = fo.get_consumer_blocks()
+    fo.set_consumer_blocks(blocks)
+    try:
+        M, N, K, cus, sizes = SMALL[name]
+        w = workloads.WORKLOADS[name].with_shape(M, N, K)
+        say(f"[consumer blocks] blocks={blocks} {w.name}")
+        inp = workloads.make_inputs(w)
+        plan, o = plan_for(w, inp, num_cus=cus, sizes=list(sizes))
+        check(w, inp, plan, o)
+    finally:
+        fo.set_consumer_blocks(old)

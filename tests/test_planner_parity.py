@@ -161,3 +161,23 @@ def test_header_symbols_are_exported():
     L = fo.lib()
     missing = [n for n in sorted(names) if not hasattr(L, n)]
     assert not missing, missing
+
+
+def test_process_wide_settings_validate_and_round_trip():
+    # host-side setters only: no device work
+    old_modes, old_blocks = fo.get_sync_mode(), fo.get_consumer_blocks()
+    try:
+        for bad in (0, 257, -3):
+            with pytest.raises(fo.FoError) as e:
+                fo.set_consumer_blocks(bad)
+            assert e.value.status == -1
+        assert fo.get_consumer_blocks() == old_blocks
+        fo.set_consumer_blocks(7)
+        assert fo.get_consumer_blocks() == 7
+        with pytest.raises(fo.FoError):
+            fo.set_sync_mode(3, 0)
+        fo.set_sync_mode(1, 0)
+        assert fo.get_sync_mode() == (1, 0)
+    finally:
+        fo.set_consumer_blocks(old_blocks)
+        fo.set_sync_mode(*old_modes)

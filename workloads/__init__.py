@@ -82,14 +82,14 @@ WORKLOADS = {
                     "simulated peer partial), groups from the planner"),
     "rs_8192x8192x3584": Workload(
         name="rs_8192x8192x3584", M=8192, N=8192, K=3584, dtype=FP16,
-        tile_m=256, tile_n=128, order="xcd", pattern=SUBTILE, seed=2,
+        tile_m=256, tile_n=256, order="xcd", pattern=SUBTILE, seed=2,
         dist="uniform", num_dest=4, sweep=(1, 2, 4, 8),
         description="MLP down-projection shard (hidden 8192, FFN 28672/8), "
                     "ReduceScatter stand-in: subtile k plus peer into one of 4 "
                     "seeded destination slot buffers"),
     "ar_rmsnorm_16384x4096x3584_bf16": Workload(
         name="ar_rmsnorm_16384x4096x3584_bf16", M=16384, N=4096, K=3584,
-        dtype=BF16, tile_m=256, tile_n=128, order="xcd", pattern=TILE, seed=3,
+        dtype=BF16, tile_m=256, tile_n=256, order="xcd", pattern=TILE, seed=3,
         dist="normal", num_dest=2, bias=True, rmsnorm=True, gamma=True,
         description="long-prefill shard, AllReduce stand-in, restore fused "
                     "with bias add and RMSNorm over N=4096"),
