@@ -58,6 +58,7 @@ def parse():
     ap.add_argument("--tile", default=None, help="override the workload's output tile, e.g. 256x256")
     ap.add_argument("--consumer-blocks", type=int, default=None,
                     help="cap of every consumer launch's grid (1..256)")
+    ap.add_argument("--serial", action="store_true", help="step phase: run the consumers on the GEMM stream")
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
@@ -100,6 +101,32 @@ def time_loop(torch, fn, iters, warmup, stream):
     e1.record(stream)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) * 1000.0 / iters      # us per iteration
+
+
+def time_gemm(torch, plan, dp, b, stream, iters, warmup, signal=True):
+    """Mean time of one GEMM launch (us), each bracketed by its own event
+    pair; with signal=True the counters (group counters and the GEMM's
+    tile-position counters) are zeroed before every launch, outside the
+    events."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(iters)]
+
+    def one(pair=None):
+        if signal:
+            fo.reset_counters(b.counters, plan.num_counters, stream)
+        if pair:
+            pair[0].record(stream)
+        fo.gemm_signal_reorder(plan, dp, b.A, b.W, b.C, b.counters if signal else None, stream)
+        if pair:
+            pair[1].record(stream)
+
+    for _ in range(warmup):
+        one()
+    torch.cuda.synchronize()
+    for k in range(iters):
+        one(ev[k])
+    torch.cuda.synchronize()
+    return float(np.mean([a.elapsed_time(c) * 1000.0 for a, c in ev]))
 
 
 def make_plan(w, inp, num_cus, sizes=None, pattern=None, gemm_us=0.0, curve=None):
@@ -230,8 +257,7 @@ def main():
         print(json.dumps({"phase": "copy", "bytes_read": 2 * n, "bytes_written": 2 * n, "us": us}))
         return
     if args.phase == "gemm":
-        us = time_loop(torch, lambda: fo.gemm_signal_reorder(base_plan, dp_base, b.A, b.W, b.C, b.counters, s1),
-                       args.steps, args.warmup, s1)
+        us = time_gemm(torch, base_plan, dp_base, b, s1, args.steps, args.warmup)
         print(json.dumps({"phase": "gemm", "us": us, "tflops": flops / us / 1e6}))
         return
 
@@ -244,17 +270,17 @@ def main():
         plan = make_plan(w, inp, num_cus, sizes=sizes)
         dp = dev_plan(torch, plan)
         torch.cuda.synchronize()
-        step_us, gemm_mean_us, gemm_med_us, wall = timed_steps(torch, w, plan, dp, b, s1, s2, args.steps,
+        step_us, gemm_mean_us, gemm_med_us, wall = timed_steps(torch, w, plan, dp, b, s1,
+                                                               s1 if args.serial else s2, args.steps,
                                                                args.warmup)
-        print(json.dumps({"phase": "step", "groups": sizes, "step_us": round(step_us, 2),
+        print(json.dumps({"phase": "step", "groups": sizes, "serial": args.serial,
+                          "consumer_blocks": fo.get_consumer_blocks(), "step_us": round(step_us, 2),
                           "gemm_us": round(gemm_mean_us, 2), "gemm_tflops": round(flops / gemm_mean_us / 1e6, 2)}))
         return
     if args.phase == "all":
         log("plain GEMM / signaled GEMM")
-        plain_us = time_loop(torch, lambda: fo.gemm_signal_reorder(plan_rm, None, b.A, b.W, b.C, None, s1),
-                             100, 10, s1)
-        sig_us = time_loop(torch, lambda: fo.gemm_signal_reorder(base_plan, dp_base, b.A, b.W, b.C, b.counters, s1),
-                           100, 10, s1)
+        plain_us = time_gemm(torch, plan_rm, None, b, s1, 100, 10, signal=False)
+        sig_us = time_gemm(torch, base_plan, dp_base, b, s1, 100, 10)
         log("consumer curve")
         n_all = w.M * w.N
         xs, ys = consumer_curve(torch, w, b, s1, n_all)
@@ -295,8 +321,7 @@ def main():
     default_modes = fo.get_sync_mode()
     for pm, cm in ((0, 0), (1, 1), (2, 2)):
         fo.set_sync_mode(pm, cm)
-        sg = time_loop(torch, lambda: fo.gemm_signal_reorder(base_plan, dp_base, b.A, b.W, b.C, b.counters, s1),
-                       50, 5, s1)
+        sg = time_gemm(torch, base_plan, dp_base, b, s1, 50, 5)
         us, gm, _, _ = timed_steps(torch, w, plan, dp, b, s1, s2, max(10, args.steps // 2), 3)
         sync_variants[f"{pm}{cm}"] = {"signaled_alone_us": round(sg, 2), "overlapped_step_us": round(us, 2),
                                       "overlapped_gemm_us": round(gm, 2)}
@@ -312,17 +337,23 @@ def main():
     fo.set_consumer_blocks(default_blocks)
 
     # ---- consistency at full size: overlapped vs serialized output bits ----
+    # (every buffer the step writes is poisoned first; 0xFFFF is a NaN)
+    for buf in (b.C, b.dst, b.out):
+        buf.fill_(-1)
     run_step(torch, w, plan, dp, b, s1, s1)
     torch.cuda.synchronize()
-    ref_out = b.out.clone()
-    ref_dst = b.dst.clone()
-    b.out.fill_(-1)
-    b.dst.fill_(-1)
+    ref_C, ref_dst, ref_out = b.C.clone(), b.dst.clone(), b.out.clone()
+    for buf in (b.C, b.dst, b.out):
+        buf.fill_(-1)
+    b.status.zero_()
     run_step(torch, w, plan, dp, b, s1, s2)
     torch.cuda.synchronize()
-    consistent = bool(torch.equal(ref_out, b.out) and torch.equal(ref_dst, b.dst))
+    consistent = bool(torch.equal(ref_out, b.out) and torch.equal(ref_dst, b.dst) and torch.equal(ref_C, b.C))
     if not consistent:
-        raise RuntimeError("overlapped and serialized runs disagree")
+        raise RuntimeError(
+            "overlapped and serialized runs disagree: C' %d, dst %d, out %d differing elements, status %d" % (
+                int((ref_C != b.C).sum()), int((ref_dst != b.dst).sum()), int((ref_out != b.out).sum()),
+                int(b.status.cpu()[0])))
 
     # ---- post-reorder vs the same kernel on an identity map (Table 5 analogue)
     post_us = time_loop(torch, lambda: fo.post_reorder(plan, dp, b.dst, b.out, b.bias, b.gamma, w.eps,

@@ -148,6 +148,10 @@ int32_t fo_plan_num_tiles(const fo_plan* plan);
 int32_t fo_plan_wave_width(const fo_plan* plan);      /* W                        */
 int32_t fo_plan_num_waves(const fo_plan* plan);       /* T                        */
 int32_t fo_plan_num_groups(const fo_plan* plan);      /* P                        */
+/* Length of the counters array of a signalling run: P group counters, then
+ * FO_DISPENSER_WORDS tile-position counters of the GEMM. */
+#define FO_DISPENSER_WORDS 8
+int32_t fo_plan_num_counters(const fo_plan* plan);    /* P + FO_DISPENSER_WORDS   */
 const int32_t* fo_plan_group_sizes(const fo_plan* plan);   /* [P], in the plan's unit */
 const int32_t* fo_plan_order(const fo_plan* plan);         /* [tiles] position -> tile */
 const int32_t* fo_plan_tile_to_slot(const fo_plan* plan);  /* [tiles] the reorder map  */
@@ -207,14 +211,22 @@ fo_status fo_plan_to_device(const fo_plan* plan, void* dev_buf, size_t bytes, vo
  *             (tm, tn) in slot s goes to subtoken pool_off[b] +
  *             pool_base[s*B+b] + (rank of row r among rows of tile row tm
  *             bound for b), b = row_bucket[tm*tile_m + r].
- * counters: [P] uint32, zeroed by the caller before the launch and before any
- * consumer of this run starts (see fo_reset_counters); NULL = no signalling.
- * When a tile's stores are complete, one workgroup-level agent-scope
- * release increment is made on counters[group of its slot]; when the GEMM
- * is done, counters[j] == target_j for every j.
+ * counters: fo_plan_num_counters(plan) = P + FO_DISPENSER_WORDS uint32,
+ * zeroed by the caller before the launch and before any consumer of this run
+ * starts (see fo_reset_counters); NULL = no signalling. When a tile's stores
+ * are complete, one workgroup-level agent-scope release increment is made on
+ * counters[group of its slot]; when the GEMM is done, counters[j] ==
+ * target_j for every j < P. counters[P ..] hand out tile positions to the
+ * GEMM's workgroups (their final values are unspecified).
+ * The GEMM runs min(tiles, W) persistent workgroups (W = the plan's wave
+ * width). With counters, each takes its next dispatch position from an
+ * atomic counter when it finishes a tile, so positions start in increasing
+ * order and a workgroup that is not yet scheduled (its compute unit busy
+ * with other work) holds no tile back; without counters, workgroup b
+ * computes positions b, b + grid, b + 2*grid, ...
  * dev_plan: the plan's device image (fo_plan_to_device).
  * Errors: FO_ERR_ARG, FO_ERR_SHAPE (K % 64), FO_ERR_UNSUPPORTED (tile shape
- * other than 256x128 / 64x64), FO_ERR_HIP (launch failure).
+ * other than 256x128 / 256x256 / 64x64), FO_ERR_HIP (launch failure).
  */
 fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan,
                                  const void* A, const void* W, void* C_out,
@@ -226,14 +238,17 @@ fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan,
  * the group's count reaches its size; the communication itself only sees a
  * contiguous buffer).
  *
- * Waits until *counter >= target (agent-scope acquire), then for i < len:
+ * Two launches on `stream`: a one-wave wait kernel that polls until
+ * *counter >= target, then the streaming kernel (agent-scope acquire), which
+ * for i < len computes:
  *   peer != NULL:  dst[i] = RNE(src[i] + peer[i])   (AllReduce/ReduceScatter
  *                  of this GPU's partial with one peer partial)
  *   peer == NULL:  dst[i] = src[i]                  (All-to-All copy)
- * counter == NULL: no wait. The wait is bounded (fo_set_poll_timeout_us); on
- * timeout the segment is not written and *status_word (if non-NULL, device
- * uint32, caller-zeroed) gets bit 0 set. Buffers must not overlap. Any
- * alignment works; 16-byte-aligned pointers take the vector path.
+ * counter == NULL: no wait (one launch). The wait is bounded
+ * (fo_set_poll_timeout_us); on timeout the segment is not written and
+ * *status_word (if non-NULL, device uint32, caller-zeroed) gets bit 0 set.
+ * Buffers must not overlap. Any alignment works; 16-byte-aligned pointers
+ * take the vector path.
  * Errors: FO_ERR_ARG (null src/dst with len > 0, len < 0, bad dtype).
  */
 fo_status fo_consume_group(const void* src, const void* peer, void* dst, int64_t len,
@@ -268,15 +283,16 @@ fo_status fo_reset_counters(uint32_t* counters, int32_t n, void* stream);
  *   gemm_stream: reset counters + status -> event E0 -> GEMM (signalling)
  *   comm_stream: wait E0 -> one consumer launch per group -> event E1
  *   gemm_stream: wait E1 -> fo_post_reorder (if out != NULL)
- * A group's consumer launch waits once for the group's counter and then
- * does what fo_consume_group does for each of the group's plan segments
- * (fo_plan_segments: 1, R or B of them). Every group but the last uses at
- * most fo_get_consumer_blocks() workgroups; the last group, which runs
- * after the GEMM, uses up to 256.
+ * A group's consumer is one wait kernel on the group's counter and one
+ * streaming kernel that does what fo_consume_group does for each of the
+ * group's plan segments (fo_plan_segments: 1, R or B of them). Every group
+ * but the last uses at most fo_get_consumer_blocks() workgroups; the last
+ * group, which runs after the GEMM, uses up to 256.
  * With comm_stream == gemm_stream (or NULL) the same work runs serialized.
  * Buffers: C_out (GEMM output, see fo_gemm_signal_reorder), peer (NULL for
  * All-to-All; else the peer's partial in C_out's layout), dst
- * (fo_plan_dest_elems), out ([M, N] or NULL), counters [P], status_word [1].
+ * (fo_plan_dest_elems), out ([M, N] or NULL), counters
+ * [fo_plan_num_counters], status_word [1].
  * gemm_begin_event / gemm_end_event: optional caller-owned hipEvent_t (as
  * void*) recorded on gemm_stream right before and after the GEMM launch, so
  * a caller can time the GEMM inside the overlapped run; NULL = none.

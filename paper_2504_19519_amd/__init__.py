@@ -82,7 +82,7 @@ def lib() -> ctypes.CDLL:
     pi64 = ctypes.POINTER(ctypes.c_int64)
     L.fo_plan_groups.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Grouping), ctypes.POINTER(vp)]
     L.fo_plan_destroy.argtypes = [vp]
-    for name in ("num_tiles", "wave_width", "num_waves", "num_groups", "num_segments"):
+    for name in ("num_tiles", "wave_width", "num_waves", "num_groups", "num_counters", "num_segments"):
         f = getattr(L, f"fo_plan_{name}")
         f.argtypes, f.restype = [vp], i32
     for name in ("group_sizes", "order", "tile_to_slot", "group_first", "group_targets",
@@ -203,6 +203,11 @@ class Plan:
     def T(self) -> int: return lib().fo_plan_num_waves(self._h)
     @property
     def P(self) -> int: return lib().fo_plan_num_groups(self._h)
+    @property
+    def num_counters(self) -> int:
+        """Length of the zeroed counters array a signalling GEMM needs (P group
+        counters, then the GEMM's tile-position counters)."""
+        return lib().fo_plan_num_counters(self._h)
     @property
     def sizes(self) -> np.ndarray: return self._arr(lib().fo_plan_group_sizes, self.P)
     @property

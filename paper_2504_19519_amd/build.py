@@ -6,7 +6,9 @@ The library is built in-tree so that it travels with the source tree:
 from __future__ import annotations
 
 import concurrent.futures
+import json
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -16,6 +18,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OBJ = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libfo.so")
+USAGE = os.path.join(OBJ, "resource_usage.json")
 SOURCES = ["plan.cpp", "gemm.hip", "consume.hip", "post.hip", "runtime.hip"]
 ARCH = "gfx950"
 
@@ -35,19 +38,44 @@ def common_flags():
             "-Wno-unused-command-line-argument"]
 
 
-def _compile(src: str) -> str:
+def _compile(src: str):
     obj = os.path.join(OBJ, os.path.basename(src) + ".o")
     cmd = [hipcc()] + common_flags() + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    if src.endswith(".hip"):
+        cmd.append("-Rpass-analysis=kernel-resource-usage")
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    return obj
+    return obj, _resource_usage(r.stderr)
+
+
+def _resource_usage(text: str) -> dict:
+    """Per-kernel registers and LDS from the compiler's resource remarks."""
+    out, name = {}, None
+    for line in text.splitlines():
+        m = re.search(r"remark:\s+Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            out[name] = {}
+            continue
+        m = re.search(r"remark:\s+(VGPRs|AGPRs|VGPRs Spill|LDS Size \[bytes/block\]|Occupancy \[waves/SIMD\]): (\d+)", line)
+        if m and name:
+            key = {"VGPRs": "vgpr", "AGPRs": "agpr", "VGPRs Spill": "vgpr_spill",
+                   "LDS Size [bytes/block]": "lds", "Occupancy [waves/SIMD]": "occupancy"}[m.group(1)]
+            out[name][key] = int(m.group(2))
+    return out
 
 
 def build(verbose: bool = False) -> str:
     os.makedirs(OBJ, exist_ok=True)
     with concurrent.futures.ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 4)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
+        results = list(ex.map(_compile, SOURCES))
+    objs = [o for o, _ in results]
+    usage = {}
+    for _, u in results:
+        usage.update(u)
+    with open(USAGE, "w") as f:
+        json.dump(usage, f, indent=1, sort_keys=True)
     tmp = LIB + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)

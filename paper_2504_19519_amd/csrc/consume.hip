@@ -5,15 +5,17 @@
 //
 // One launch handles the contiguous segments of one group (one segment for a
 // plain (ptr, len) call; the R or B destination pieces of a group for the
-// ReduceScatter and All-to-All stand-ins): every workgroup waits for the
-// group's counter (relaxed agent-scope polls with s_sleep; then an
-// agent-scope acquire, or device-coherent loads of the segment, see
-// fo_sync_mode), then streams each segment with a grid-stride loop:
+// ReduceScatter and All-to-All stand-ins). As in Section 5 (a signalling
+// kernel holds back the communication call of a group until the group's
+// count reaches its tile count), a one-wave wait kernel polls the group's
+// counter, and the streaming kernel that follows it on the stream takes an
+// agent-scope acquire (or reads with device-coherent loads, see
+// fo_sync_mode) and streams each segment with a grid-stride loop:
 //   dst = RNE(src + peer)   AllReduce / ReduceScatter of two partials
 //   dst = src               All-to-All (copy to the receive buffer)
-// The wait is bounded by a wall-clock limit; on timeout the workgroup writes
-// nothing and raises bit 0 of the status word, so a missing signal can never
-// hang the device.
+// The wait is bounded by a wall-clock limit; on timeout the streaming
+// workgroups write nothing and bit 0 of the status word is raised, so a
+// missing signal can never hang the device.
 //
 // A consumer workgroup holds 4 bytes of LDS and at most 56 registers per
 // lane, so it fits beside a GEMM workgroup on the same compute unit (the
@@ -32,28 +34,41 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kUnroll = 4;
 
-// Wait until *counter >= target. Thread 0 polls with relaxed agent-scope
-// loads (device-coherent, no cache invalidation) and sleeps between polls.
+// The wait of a launch runs in a kernel of its own, one workgroup of one
+// wave, ahead of the streaming kernel on the same stream: one lane polls the
+// counter with relaxed agent-scope loads (device-coherent, no cache
+// invalidation) and sleeps between polls. Polling from every streaming
+// workgroup instead (hundreds of pollers on one cache line) measurably slows
+// a GEMM running beside it; one poller does not. The streaming kernel starts
+// only when the wait kernel has ended. The wait is bounded by a wall-clock
+// limit; on timeout bit 0 of the status word is raised.
+__global__ __launch_bounds__(64) void wait_kernel(const uint32_t* counter, uint32_t target, uint32_t* status,
+                                                  uint64_t timeout_ticks) {
+    if (threadIdx.x != 0) return;
+    if (__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target) return;
+    const uint64_t t0 = wall_clock64();
+    while (__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+        __builtin_amdgcn_s_sleep(8);
+        if (wall_clock64() - t0 > timeout_ticks) {
+            if (status) __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return;
+        }
+    }
+}
+
+// Start of a streaming workgroup: one read of the counter (the wait kernel
+// has returned, so it normally holds the target already; if the wait timed
+// out the workgroup raises the status bit and writes nothing), then the
+// acquire the mode needs.
 // SYNC == FENCE_ALL: thread 0 and then every wave take an agent-scope
 // acquire (cache invalidation); FENCE_ONE: thread 0 only (its invalidation
 // covers the CU's L1 and the chiplet's L2 that the whole workgroup uses);
 // COHERENT: no acquire, the data is then read with device-coherent loads.
 template <int SYNC>
-__device__ __forceinline__ bool wait_counter(const uint32_t* counter, uint32_t target,
-                                             uint32_t* status, uint64_t timeout_ticks) {
+__device__ __forceinline__ bool check_counter(const uint32_t* counter, uint32_t target, uint32_t* status) {
     __shared__ int s_ok;
     if (threadIdx.x == 0) {
-        int ok = 1;
-        if (__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-            const uint64_t t0 = wall_clock64();
-            while (__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-                __builtin_amdgcn_s_sleep(8);
-                if (wall_clock64() - t0 > timeout_ticks) {
-                    ok = 0;
-                    break;
-                }
-            }
-        }
+        const int ok = __hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target;
         if (ok) {
             if constexpr (SYNC != FO_SYNC_COHERENT) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         } else if (status) {
@@ -184,12 +199,12 @@ __device__ __forceinline__ void stream_elem(const uint16_t* __restrict__ src, co
 
 enum { kPathVec16 = 0, kPathCoherent8 = 1, kPathElem = 2 };
 
-// SYNC: how the wait publishes the group to the workgroup (wait_counter).
+// SYNC: how the group is published to the workgroup (check_counter).
 // PATH: kPathCoherent8 goes with SYNC == COHERENT; kPathElem (unaligned
 // buffers) waits with FENCE_ALL in every mode, since plain loads follow.
 template <int DT, bool SUM, int SYNC, int PATH>
 __global__ __launch_bounds__(kThreads) void consume_kernel(const ConsumeArgs a) {
-    if (a.counter && !wait_counter<SYNC>(a.counter, a.target, a.status, a.timeout_ticks)) return;
+    if (a.counter && !check_counter<SYNC>(a.counter, a.target, a.status)) return;
     for (int k = 0; k < a.nseg; ++k) {
         const ConsumeSegment g = a.seg[k];
         const uint16_t* src = a.src + g.src_off;
@@ -236,6 +251,11 @@ hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blo
     if (blocks < 1) blocks = 1;
     if (blocks > max_blocks) blocks = max_blocks;
     const dim3 g((unsigned)blocks), b(kThreads);
+    if (a.counter) {
+        hipLaunchKernelGGL(wait_kernel, dim3(1), dim3(64), 0, s, a.counter, a.target, a.status, a.timeout_ticks);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     const bool sum = a.peer != nullptr;
     if (dtype == FO_FP16) {
         if (sum) launch_variant<FO_FP16, true>(sync, path, g, b, s, a);

@@ -22,9 +22,13 @@ struct GemmArgs {
     const int32_t* pool_base;
     const int32_t* pool_off;
     uint32_t* counters;            // [P] or null
+    uint32_t* dispenser;           // [num_dispensers] zeroed position counters, or null
+    int32_t num_dispensers;        // D >= 1 (with a dispenser)
     int32_t sync;                  // fo_sync_mode of the producer side
 };
 
+// grid: number of persistent workgroups (at most the number of tiles; with
+// a dispenser, a multiple of num_dispensers).
 hipError_t launch_gemm(int dtype, int tile_m, int tile_n, const GemmArgs& a, int grid, hipStream_t s);
 bool gemm_tile_supported(int tile_m, int tile_n);
 

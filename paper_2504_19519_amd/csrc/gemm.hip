@@ -152,22 +152,32 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
     __shared__ __attribute__((aligned(1024))) char st1[T::kStage];
     __shared__ __attribute__((aligned(1024))) char st2[STAGES == 3 ? T::kStage : 1024];
     __shared__ int64_t row_off[BM];
+    __shared__ int s_pos;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar registers
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-    const int p = blockIdx.x;
-    const int tile = tile_of_position(p, a.tiles_m, a.tiles_n, a.order, a.group_m, a.num_xcds);
-    const int tm = tile / a.tiles_n, tn = tile - (tile / a.tiles_n) * a.tiles_n;
     const int64_t K = a.K;
+    const int tiles = a.tiles_m * a.tiles_n;
 
-    // Plan lookups needed only by the epilogue: issued now, consumed later.
-    const int slot = a.tile_to_slot ? a.tile_to_slot[tile] : p;
-    int bucket = 0, rank = 0;
-    if (a.pattern == FO_PATTERN_SUBTOKEN && tid < BM) {
-        bucket = a.row_bucket[tm * BM + tid];
-        rank = a.row_rank[tm * BM + tid];
+    // Persistent workgroups. Positions are handed out in increasing order:
+    // with a dispenser, workgroup b takes positions d, d + D, d + 2D, ... of
+    // its class d = b % D from an atomic counter shared by the class (so a
+    // position always runs on the chiplet the dispatch order meant it for,
+    // and a workgroup that is never scheduled holds no position back);
+    // without one, workgroup b takes b, b + grid, b + 2 grid, ...
+    const int D = a.num_dispensers;
+    const int cls = a.dispenser ? (int)(blockIdx.x % (unsigned)D) : 0;
+    auto claim = [&]() -> int {
+        return cls + D * (int)__hip_atomic_fetch_add(a.dispenser + cls, 1u, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+    };
+    int p = (int)blockIdx.x;
+    if (a.dispenser) {
+        if (tid == 0) s_pos = claim();
+        __syncthreads();
+        p = __builtin_amdgcn_readfirstlane(s_pos);   // uniform: scalar registers
     }
 
     // A load instruction fills one 1 KB block = 8 rows: lane l writes slot
@@ -182,9 +192,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
     for (int i = 0; i < T::kAI; ++i) voffA[i] = voff(wave * T::kAI + i);
 #pragma unroll
     for (int i = 0; i < T::kBI; ++i) voffB[i] = voff(wave * T::kBI + i);
-    const uint16_t* Ablk = a.A + (int64_t)tm * BM * K;
-    const uint16_t* Wblk = a.W + (int64_t)tn * BN * K;
     const int KT = (int)(K / kBK);
+    const uint16_t* Ablk = a.A;
+    const uint16_t* Wblk = a.W;
     // Tiles past the last k step are "loaded" through empty resources: the
     // loads return zeros without touching memory, so every step issues the
     // same loads and the wait counts stay uniform (no branches).
@@ -196,12 +206,6 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
     };
 
     f32x16_t acc[MI][NJ];
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NJ; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     // Fragment addressing: lane l feeds row (l % 32) of a 32-row block with
     // the 8 consecutive k values of chunk 2*kk + l/32 of the 16-wide step kk.
@@ -260,136 +264,183 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
         __builtin_amdgcn_sched_barrier(0);
     };
 
-    issue(0, st0);
-    issue(1, st1);
-    if constexpr (STAGES == 3) issue(2, st2);
-    wait_and_barrier<(STAGES - 1) * T::kLoads>();
-    load_frags(st0, 0, fa0, fb0);
-    int kt = 0;
-    if constexpr (STAGES == 3) {
-        for (; kt + 3 <= KT; kt += 3) {      // tile t lives in stage t % 3
-            step(kt, st0, st1);
-            step(kt + 1, st1, st2);
-            step(kt + 2, st2, st0);
-        }
-        if (kt < KT) step(kt, st0, st1);
-        if (kt + 1 < KT) step(kt + 1, st1, st2);
-    } else {
-        for (; kt + 2 <= KT; kt += 2) {      // tile t lives in stage t % 2
-            step(kt, st0, st1);
-            step(kt + 1, st1, st0);
-        }
-        if (kt < KT) step(kt, st0, st1);
-    }
-    wait_and_barrier<0>();    // no load may still be writing LDS
-    __syncthreads();          // operand stages are reused for the output tile
-
-    // ---- epilogue -------------------------------------------------------
-    // Destination of row `tid` of the tile, by pattern.
-    if (tid < BM) {
-        const int r = tid;
-        int64_t off;
-        if (a.pattern == FO_PATTERN_ROWMAJOR) {
-            off = ((int64_t)tm * BM + r) * a.N + (int64_t)tn * BN;
-        } else if (a.pattern == FO_PATTERN_TILE) {
-            off = ((int64_t)slot * BM + r) * BN;
-        } else if (a.pattern == FO_PATTERN_SUBTILE) {
-            const int h = BM / a.num_dest;
-            const int k = r / h, rr = r - (r / h) * h;
-            const int j = a.slot_group[slot];
-            const int64_t f0 = a.group_first[j];
-            const int64_t nj = a.group_first[j + 1] - f0;
-            off = f0 * BM * BN + ((int64_t)k * nj + (slot - f0)) * h * BN + (int64_t)rr * BN;
-        } else {
-            const int B = a.num_dest;
-            off = ((int64_t)a.pool_off[bucket] + a.pool_base[(int64_t)slot * B + bucket] + rank) * BN;
-        }
-        row_off[r] = off;
-    }
-
-    // Staging row r of a pass ([0, kRowsPerPass)): the first half of the
-    // rows in stage 0, the second half in stage 1.
+    // Staging row r of an output pass ([0, kRowsPerPass)): the first half of
+    // the rows in stage 0, the second half in stage 1.
     constexpr int kHalf = T::kRowsPerPass / 2;
     auto crow = [&](int r) -> uint16_t* {
         return reinterpret_cast<uint16_t*>(r < kHalf ? st0 + r * T::kLDC * 2 : st1 + (r - kHalf) * T::kLDC * 2);
     };
     const bool coherent = a.counters && a.sync == FO_SYNC_COHERENT;
+
+    while (p < tiles) {
+        const int tile = tile_of_position(p, a.tiles_m, a.tiles_n, a.order, a.group_m, a.num_xcds);
+        const int tm = tile / a.tiles_n, tn = tile - (tile / a.tiles_n) * a.tiles_n;
+        Ablk = a.A + (int64_t)tm * BM * K;
+        Wblk = a.W + (int64_t)tn * BN * K;
+
+        // Plan lookups needed only by the epilogue: issued now, consumed later.
+        const int slot = a.tile_to_slot ? a.tile_to_slot[tile] : p;
+        int bucket = 0, rank = 0;
+        if (a.pattern == FO_PATTERN_SUBTOKEN && tid < BM) {
+            bucket = a.row_bucket[tm * BM + tid];
+            rank = a.row_rank[tm * BM + tid];
+        }
+
 #pragma unroll
-    for (int pass = 0; pass < T::kPasses; ++pass) {
-        const int r0 = pass * T::kRowsPerPass;
-        // accumulators of the waves whose rows are in this pass -> staging
-        if (wm * WTM >= r0 && wm * WTM < r0 + T::kRowsPerPass) {
+        for (int i = 0; i < MI; ++i)
 #pragma unroll
-            for (int i = 0; i < MI; ++i) {
-                const int m = wm * WTM - r0 + i * 32 + (lane & 31);
+            for (int j = 0; j < NJ; ++j)
 #pragma unroll
-                for (int j = 0; j < NJ; ++j) {
+                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+        issue(0, st0);
+        issue(1, st1);
+        if constexpr (STAGES == 3) issue(2, st2);
+        wait_and_barrier<(STAGES - 1) * T::kLoads>();
+        load_frags(st0, 0, fa0, fb0);
+        int kt = 0;
+        if constexpr (STAGES == 3) {
+            for (; kt + 3 <= KT; kt += 3) {      // tile t lives in stage t % 3
+                step(kt, st0, st1);
+                step(kt + 1, st1, st2);
+                step(kt + 2, st2, st0);
+            }
+            if (kt < KT) step(kt, st0, st1);
+            if (kt + 1 < KT) step(kt + 1, st1, st2);
+        } else {
+            for (; kt + 2 <= KT; kt += 2) {      // tile t lives in stage t % 2
+                step(kt, st0, st1);
+                step(kt + 1, st1, st0);
+            }
+            if (kt < KT) step(kt, st0, st1);
+        }
+        wait_and_barrier<0>();    // no load may still be writing LDS
+        __syncthreads();          // operand stages are reused for the output tile
+
+        // ---- epilogue ---------------------------------------------------
+        // The epilogue's thread coordinates go through an opaque copy, so
+        // that its address arithmetic stays here instead of being hoisted
+        // out of the tile loop (where it would hold registers through the
+        // main loop).
+        int tid_e = tid;
+        asm volatile("" : "+v"(tid_e));
+        const int lane_e = tid_e & 63, wave_e = __builtin_amdgcn_readfirstlane(tid_e >> 6);
+        const int wm_e = wave_e / WAVES_N, wn_e = wave_e % WAVES_N;
+        // Destination of row `tid` of the tile, by pattern.
+        if (tid < BM) {
+            const int r = tid;
+            int64_t off;
+            if (a.pattern == FO_PATTERN_ROWMAJOR) {
+                off = ((int64_t)tm * BM + r) * a.N + (int64_t)tn * BN;
+            } else if (a.pattern == FO_PATTERN_TILE) {
+                off = ((int64_t)slot * BM + r) * BN;
+            } else if (a.pattern == FO_PATTERN_SUBTILE) {
+                const int h = BM / a.num_dest;
+                const int k = r / h, rr = r - (r / h) * h;
+                const int j = a.slot_group[slot];
+                const int64_t f0 = a.group_first[j];
+                const int64_t nj = a.group_first[j + 1] - f0;
+                off = f0 * BM * BN + ((int64_t)k * nj + (slot - f0)) * h * BN + (int64_t)rr * BN;
+            } else {
+                const int B = a.num_dest;
+                off = ((int64_t)a.pool_off[bucket] + a.pool_base[(int64_t)slot * B + bucket] + rank) * BN;
+            }
+            row_off[r] = off;
+        }
+
+        // The next position is claimed now; the atomic's latency hides
+        // behind this tile's stores.
+        int next = p + (int)gridDim.x;
+        if (a.dispenser && tid == 0) next = claim();
+
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const int n = wn * WTN + j * 32 + q * 8 + (lane >> 5) * 4;
-                        u32x2_t v;
-                        v[0] = pack2<DT>(acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]);
-                        v[1] = pack2<DT>(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-                        *reinterpret_cast<u32x2_t*>(crow(m) + n) = v;
+        for (int pass = 0; pass < T::kPasses; ++pass) {
+            const int r0 = pass * T::kRowsPerPass;
+            // accumulators of the waves whose rows are in this pass -> staging
+            if (wm_e * WTM >= r0 && wm_e * WTM < r0 + T::kRowsPerPass) {
+#pragma unroll
+                for (int i = 0; i < MI; ++i) {
+                    const int m = wm_e * WTM - r0 + i * 32 + (lane_e & 31);
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j) {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const int n = wn_e * WTN + j * 32 + q * 8 + (lane_e >> 5) * 4;
+                            u32x2_t v;
+                            v[0] = pack2<DT>(acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]);
+                            v[1] = pack2<DT>(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+                            *reinterpret_cast<u32x2_t*>(crow(m) + n) = v;
+                        }
                     }
                 }
             }
-        }
-        __syncthreads();
-        if (coherent) {
-            // Device-coherent 8-byte stores (written through to the point all
-            // chiplets share): no cache write-back is needed before the signal.
-            constexpr int LPR = BN / 4;             // lanes per row (8 bytes each)
-            constexpr int RPI = LPR >= 64 ? 1 : 64 / LPR;   // rows per wave instruction
-            constexpr int CPL = LPR >= 64 ? LPR / 64 : 1;   // 8-byte columns per lane
-            const int lr = LPR >= 64 ? 0 : lane / LPR;
-            const int lc = LPR >= 64 ? lane : lane % LPR;
+            __syncthreads();
+            if (coherent) {
+                // Device-coherent 8-byte stores (written through to the point
+                // all chiplets share): no cache write-back is needed before
+                // the signal.
+                constexpr int LPR = BN / 4;             // lanes per row (8 bytes each)
+                constexpr int RPI = LPR >= 64 ? 1 : 64 / LPR;   // rows per wave_e instruction
+                constexpr int CPL = LPR >= 64 ? LPR / 64 : 1;   // 8-byte columns per lane_e
+                const int lr = LPR >= 64 ? 0 : lane_e / LPR;
+                const int lc = LPR >= 64 ? lane_e : lane_e % LPR;
 #pragma unroll 4
-            for (int r = wave * RPI + lr; r < T::kRowsPerPass; r += NW * RPI) {
+                for (int r = wave_e * RPI + lr; r < T::kRowsPerPass; r += NW * RPI) {
 #pragma unroll
-                for (int cc = 0; cc < CPL; ++cc) {
-                    const int col = lc + cc * 64;
-                    const uint64_t v = *reinterpret_cast<const uint64_t*>(crow(r) + col * 4);
-                    __hip_atomic_store(reinterpret_cast<uint64_t*>(a.C + row_off[r0 + r]) + col, v,
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    for (int cc = 0; cc < CPL; ++cc) {
+                        const int col = lc + cc * 64;
+                        const uint64_t v = *reinterpret_cast<const uint64_t*>(crow(r) + col * 4);
+                        __hip_atomic_store(reinterpret_cast<uint64_t*>(a.C + row_off[r0 + r]) + col, v,
+                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                }
+            } else {
+                constexpr int CPR = BN / 8;             // 16-byte chunks per tile row
+                constexpr int RPP = NT / CPR;           // rows per pass of the workgroup
+                const int c = tid_e % CPR;
+#pragma unroll 4
+                for (int r = tid_e / CPR; r < T::kRowsPerPass; r += RPP) {
+                    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(crow(r) + c * 8);
+                    *reinterpret_cast<u32x4_t*>(a.C + row_off[r0 + r] + c * 8) = v;
                 }
             }
-        } else {
-            constexpr int CPR = BN / 8;             // 16-byte chunks per tile row
-            constexpr int RPP = NT / CPR;           // rows per pass of the workgroup
-            const int c = tid % CPR;
-#pragma unroll 4
-            for (int r = tid / CPR; r < T::kRowsPerPass; r += RPP) {
-                const u32x4_t v = *reinterpret_cast<const u32x4_t*>(crow(r) + c * 8);
-                *reinterpret_cast<u32x4_t*>(a.C + row_off[r0 + r] + c * 8) = v;
+            if (pass + 1 < T::kPasses) __syncthreads();   // staging is refilled
+        }
+
+        if (a.counters) {
+            // Section 3.2: count the finished tile for its group once all of
+            // the tile's stores are visible to every compute unit.
+            if (coherent) {
+                // each wave waits until its write-through stores are complete
+                __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+                __syncthreads();
+                if (tid == 0)
+                    __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+            } else if (a.sync == FO_SYNC_FENCE_ALL) {
+                // every wave: release fence at agent scope (L2 write-back + wait)
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                __syncthreads();
+                if (tid == 0)
+                    __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+            } else {
+                // workgroup barrier, then one release increment (one write-back)
+                __syncthreads();
+                if (tid == 0)
+                    __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELEASE,
+                                           __HIP_MEMORY_SCOPE_AGENT);
             }
         }
-        if (pass + 1 < T::kPasses) __syncthreads();   // staging is refilled
-    }
-
-    if (!a.counters) return;
-    // Section 3.2: count the finished tile for its group once all of the
-    // tile's stores are visible to every compute unit.
-    if (coherent) {
-        // each wave waits until its write-through stores are complete
-        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        // Every wave is done with the staging tile (the next tile's loads
+        // overwrite it) before the next position is published.
         __syncthreads();
-        if (tid == 0)
-            __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-    } else if (a.sync == FO_SYNC_FENCE_ALL) {
-        // every wave: release fence at agent scope (L2 write-back + wait)
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-        __syncthreads();
-        if (tid == 0)
-            __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-    } else {
-        // workgroup barrier, then one release increment (one write-back)
-        __syncthreads();
-        if (tid == 0)
-            __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELEASE,
-                                   __HIP_MEMORY_SCOPE_AGENT);
+        if (a.dispenser) {
+            if (tid == 0) s_pos = next;
+            __syncthreads();
+            next = s_pos;
+        }
+        p = __builtin_amdgcn_readfirstlane(next);
     }
 }
 

@@ -214,8 +214,15 @@ fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan, cons
     }
     a.counters = plan->P > 0 ? counters : nullptr;
     a.sync = fo::g_sync_producer.load(std::memory_order_relaxed);
-    hipError_t e = fo::launch_gemm(plan->dtype, plan->tile_m, plan->tile_n, a, plan->tiles,
-                                   (hipStream_t)stream);
+    // Persistent grid: one workgroup per tile of a wave. Position classes
+    // follow the chiplet of the XCD dispatch order.
+    const int grid = std::min(plan->tiles, std::max(plan->W, 1));
+    if (a.counters) {
+        a.dispenser = counters + plan->P;
+        a.num_dispensers = plan->order == FO_ORDER_XCD ? std::min(plan->num_xcds, FO_DISPENSER_WORDS) : 1;
+        a.num_dispensers = std::max(1, std::min(a.num_dispensers, grid));
+    }
+    hipError_t e = fo::launch_gemm(plan->dtype, plan->tile_m, plan->tile_n, a, grid, (hipStream_t)stream);
     return e == hipSuccess ? FO_OK : fo::hip_fail("GEMM launch", e);
 }
 
@@ -320,7 +327,7 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
     hipStream_t s1 = (hipStream_t)gemm_stream, s2 = (hipStream_t)comm_stream;
     fo_status st;
     if (overlap) {
-        if ((st = fo_reset_counters(counters, plan->P, s1)) != FO_OK) return st;
+        if ((st = fo_reset_counters(counters, plan->P + FO_DISPENSER_WORDS, s1)) != FO_OK) return st;
     }
     if (status_word && (st = fo_reset_counters(status_word, 1, s1)) != FO_OK) return st;
     hipEvent_t e0 = nullptr, e1 = nullptr;

@@ -119,7 +119,7 @@ def test_reordered_output_is_permuted_plain_output(pattern, nd, dtype, sizes, ti
     plan = fo.plan_groups(M, N, K, pattern=pattern, sizes=list(sizes), **common)
     o = oracle.make_plan(M, N, tile[0], tile[1], num_cus=8, order="xcd", pattern=pattern, num_dest=nd,
                          sigma=sigma, bucket=bucket, sizes=sizes)
-    counters = zeros_u32(plan.P)
+    counters = zeros_u32(plan.num_counters)
     Cr = _gemm(plan, A, W, counters=counters, poison=dtype)
     np.testing.assert_array_equal(Cr, C[oracle.reorder_index(o)])
     np.testing.assert_array_equal(counters.cpu().numpy()[:plan.P], np.array(o.targets))

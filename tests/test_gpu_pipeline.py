@@ -46,7 +46,7 @@ def run(w, plan, d: Dev, *, overlap=True):
     C = empty16(w.M * w.N, w.dtype)
     dst = empty16(plan.dest_elems, w.dtype)
     out = empty16(w.M * w.N, w.dtype)
-    counters = zeros_u32(plan.P)
+    counters = zeros_u32(plan.num_counters)
     status = zeros_u32(1)
     s1 = torch.cuda.Stream()
     s2 = torch.cuda.Stream() if overlap else s1
@@ -180,7 +180,7 @@ def test_consumers_wait_for_a_delayed_gemm():
     d = Dev(w, inp, plan)
     C = empty16(w.M * w.N, w.dtype)
     dst = empty16(plan.dest_elems, w.dtype)
-    counters = zeros_u32(plan.P)
+    counters = zeros_u32(plan.num_counters)
     s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
     torch.cuda.synchronize()
     for (j, _, so, do, ln) in plan.segments:

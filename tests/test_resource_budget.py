@@ -1,0 +1,43 @@
+"""A consumer workgroup must fit on a compute unit beside a GEMM workgroup.
+
+The consumer kernels poll and stream while the persistent GEMM holds one
+workgroup per compute unit; if a consumer workgroup did not fit beside it, it
+would take the compute unit away from the GEMM for as long as it waits. The
+budget is checked on the compiler's resource report that the build writes
+(gfx950: 512 registers per SIMD lane, allocated in blocks of 8; 160 KiB of
+LDS per compute unit; a consumer workgroup has one wave per SIMD).
+"""
+import json
+import os
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+USAGE = os.path.join(ROOT, "paper_2504_19519_amd", "_build", "resource_usage.json")
+
+
+def _round8(n):
+    return (n + 7) // 8 * 8
+
+
+def _usage():
+    if not os.path.exists(USAGE):
+        pytest.fail("no resource report: build the library first (python -m paper_2504_19519_amd.build)")
+    with open(USAGE) as f:
+        return json.load(f)
+
+
+def test_consumer_fits_beside_every_gemm_kernel():
+    u = _usage()
+    gemm = {k: v for k, v in u.items() if "gemm_signal_kernel" in k}
+    cons = {k: v for k, v in u.items() if "consume_kernel" in k}
+    assert len(gemm) >= 6 and len(cons) >= 8
+    c_regs = max(_round8(v["vgpr"] + v.get("agpr", 0)) for v in cons.values())
+    c_lds = max(v["lds"] for v in cons.values())
+    for name, v in gemm.items():
+        assert v.get("vgpr_spill", 0) == 0, name
+        # waves of one GEMM workgroup per SIMD: 256 threads -> 1, 512 -> 2
+        per_simd = 2 if ("ILi2ELi4E" in name) else 1
+        regs = per_simd * _round8(v["vgpr"] + v.get("agpr", 0))
+        assert regs + c_regs <= 512, (name, regs, c_regs)
+        assert v["lds"] + c_lds <= 160 * 1024, (name, v["lds"], c_lds)
