@@ -286,8 +286,9 @@ fo_status fo_reset_counters(uint32_t* counters, int32_t n, void* stream);
  * A group's consumer is one wait kernel on the group's counter and one
  * streaming kernel that does what fo_consume_group does for each of the
  * group's plan segments (fo_plan_segments: 1, R or B of them). Every group
- * but the last uses at most fo_get_consumer_blocks() workgroups; the last
- * group, which runs after the GEMM, uses up to 256.
+ * but the last uses the grid of fo_get_consumer_grid(); the last group,
+ * which runs after the GEMM, uses up to 256 workgroups of 256 threads (as do
+ * all groups of a serialized run).
  * With comm_stream == gemm_stream (or NULL) the same work runs serialized.
  * Buffers: C_out (GEMM output, see fo_gemm_signal_reorder), peer (NULL for
  * All-to-All; else the peer's partial in C_out's layout), dst
@@ -328,14 +329,15 @@ typedef enum { FO_SYNC_FENCE_ALL = 0, FO_SYNC_FENCE_ONE = 1, FO_SYNC_COHERENT = 
 fo_status fo_set_sync_mode(int32_t producer, int32_t consumer);
 void fo_get_sync_mode(int32_t* producer, int32_t* consumer);
 
-/* Largest grid of a consumer launch that runs beside the GEMM (every
- * fo_consume_group call, and every group but the last in
- * fo_run_overlapped), in 256-thread workgroups (1 .. 256, default 256; env
- * FO_CONSUMER_BLOCKS overrides at load time). Fewer workgroups stream a
- * group more slowly but leave more of the memory system to the GEMM.
- * Process-wide; FO_ERR_ARG outside the range. */
-fo_status fo_set_consumer_blocks(int32_t max_blocks);
-int32_t fo_get_consumer_blocks(void);
+/* Grid of a consumer launch that runs beside the GEMM (every
+ * fo_consume_group call, and every group but the last in fo_run_overlapped):
+ * at most max_blocks workgroups (1 .. 256) of `threads` threads (64, 128 or
+ * 256); default 256 x 256. A smaller grid streams a group more slowly and
+ * spreads its memory traffic over more of the GEMM's run. Env
+ * FO_CONSUMER_BLOCKS / FO_CONSUMER_THREADS override at load time.
+ * Process-wide; FO_ERR_ARG outside the ranges. */
+fo_status fo_set_consumer_grid(int32_t max_blocks, int32_t threads);
+void fo_get_consumer_grid(int32_t* max_blocks, int32_t* threads);
 
 /* Upper bound of one consumer wait, in microseconds (default 2 s; env
  * FO_POLL_TIMEOUT_US overrides at load time). */

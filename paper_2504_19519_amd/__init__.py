@@ -21,7 +21,7 @@ __all__ = [
     "FoError", "Plan", "plan_groups", "gemm_signal_reorder", "consume_group",
     "post_reorder", "reset_counters", "run_overlapped", "set_poll_timeout_us",
     "get_poll_timeout_us", "device_num_cus", "set_sync_mode", "get_sync_mode",
-    "set_consumer_blocks", "get_consumer_blocks", "LIB_PATH",
+    "set_consumer_grid", "get_consumer_grid", "LIB_PATH",
     "FP16", "BF16", "TILE", "SUBTILE", "SUBTOKEN", "ROWMAJOR",
 ]
 
@@ -102,8 +102,8 @@ def lib() -> ctypes.CDLL:
                                     vp, vp, vp, vp, vp, vp]
     L.fo_set_sync_mode.argtypes, L.fo_set_sync_mode.restype = [i32, i32], ctypes.c_int
     L.fo_get_sync_mode.argtypes = [pi32, pi32]
-    L.fo_set_consumer_blocks.argtypes, L.fo_set_consumer_blocks.restype = [i32], ctypes.c_int
-    L.fo_get_consumer_blocks.argtypes, L.fo_get_consumer_blocks.restype = [], i32
+    L.fo_set_consumer_grid.argtypes, L.fo_set_consumer_grid.restype = [i32, i32], ctypes.c_int
+    L.fo_get_consumer_grid.argtypes = [pi32, pi32]
     L.fo_set_poll_timeout_us.argtypes = [i64]
     L.fo_get_poll_timeout_us.restype = i64
     L.fo_device_num_cus.argtypes = [i32, pi32]
@@ -324,14 +324,17 @@ def get_sync_mode():
     return int(p.value), int(c.value)
 
 
-def set_consumer_blocks(max_blocks: int) -> None:
-    """Cap the grid of every consumer launch at `max_blocks` 256-thread
-    workgroups (1 .. 256; process-wide)."""
-    _check(lib().fo_set_consumer_blocks(int(max_blocks)))
+def set_consumer_grid(max_blocks: int, threads: int = 64) -> None:
+    """Grid of the consumer launches that run beside the GEMM: at most
+    `max_blocks` workgroups (1..256) of `threads` threads (64, 128, 256);
+    process-wide."""
+    _check(lib().fo_set_consumer_grid(int(max_blocks), int(threads)))
 
 
-def get_consumer_blocks() -> int:
-    return int(lib().fo_get_consumer_blocks())
+def get_consumer_grid():
+    b, t = ctypes.c_int32(), ctypes.c_int32()
+    lib().fo_get_consumer_grid(ctypes.byref(b), ctypes.byref(t))
+    return int(b.value), int(t.value)
 
 
 def set_poll_timeout_us(us: int) -> None:

@@ -6,8 +6,7 @@
 
 namespace fo {
 
-// Largest consumer grid: one 256-thread workgroup (one wave per SIMD) per
-// compute unit at most.
+// Largest consumer grid: one workgroup per compute unit.
 constexpr int kMaxConsumeBlocks = 256;
 // Segments one launch can carry (a group has R or B of them).
 constexpr int kMaxConsumeSegments = 16;
@@ -31,7 +30,8 @@ struct ConsumeArgs {
 };
 
 // One launch: wait once for *counter >= target, then stream every segment.
-// max_blocks caps the grid (1 .. kMaxConsumeBlocks).
-hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blocks, hipStream_t s);
+// max_blocks caps the grid (1 .. kMaxConsumeBlocks); threads per workgroup:
+// 64, 128 or 256.
+hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blocks, int threads, hipStream_t s);
 
 }  // namespace fo

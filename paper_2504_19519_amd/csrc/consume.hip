@@ -31,7 +31,7 @@
 namespace fo {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kMaxThreads = 256;
 constexpr int kUnroll = 4;
 
 // The wait of a launch runs in a kernel of its own, one workgroup of one
@@ -113,8 +113,8 @@ __device__ __forceinline__ void stream_vec16(const uint16_t* __restrict__ src, c
     const u32x4_t* s = reinterpret_cast<const u32x4_t*>(src);
     const u32x4_t* q = reinterpret_cast<const u32x4_t*>(peer);
     u32x4_t* d = reinterpret_cast<u32x4_t*>(dst);
-    const int64_t stride = (int64_t)gridDim.x * kThreads;
-    int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     for (; i + (kUnroll - 1) * stride < n16; i += kUnroll * stride) {
         u32x4_t x[kUnroll], y[kUnroll];
 #pragma unroll
@@ -152,8 +152,8 @@ __device__ __forceinline__ void stream_coherent8(const uint16_t* __restrict__ sr
     const uint64_t* s = reinterpret_cast<const uint64_t*>(src);
     const uint64_t* q = reinterpret_cast<const uint64_t*>(peer);
     uint64_t* d = reinterpret_cast<uint64_t*>(dst);
-    const int64_t stride = (int64_t)gridDim.x * kThreads;
-    int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     auto add4 = [](uint64_t x, uint64_t y) -> uint64_t {
         u32x4_t a, b;
         a[0] = (uint32_t)x; a[1] = (uint32_t)(x >> 32); a[2] = 0; a[3] = 0;
@@ -192,8 +192,8 @@ __device__ __forceinline__ void stream_coherent8(const uint16_t* __restrict__ sr
 template <int DT, bool SUM>
 __device__ __forceinline__ void stream_elem(const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer,
                                             uint16_t* __restrict__ dst, int64_t len) {
-    const int64_t stride = (int64_t)gridDim.x * kThreads;
-    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < len; i += stride)
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += stride)
         dst[i] = SUM ? add1<DT>(src[i], peer[i]) : src[i];
 }
 
@@ -203,7 +203,7 @@ enum { kPathVec16 = 0, kPathCoherent8 = 1, kPathElem = 2 };
 // PATH: kPathCoherent8 goes with SYNC == COHERENT; kPathElem (unaligned
 // buffers) waits with FENCE_ALL in every mode, since plain loads follow.
 template <int DT, bool SUM, int SYNC, int PATH>
-__global__ __launch_bounds__(kThreads) void consume_kernel(const ConsumeArgs a) {
+__global__ __launch_bounds__(kMaxThreads) void consume_kernel(const ConsumeArgs a) {
     if (a.counter && !check_counter<SYNC>(a.counter, a.target, a.status)) return;
     for (int k = 0; k < a.nseg; ++k) {
         const ConsumeSegment g = a.seg[k];
@@ -230,7 +230,7 @@ void launch_variant(int sync, int path, dim3 g, dim3 b, hipStream_t s, const Con
 
 }  // namespace
 
-hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blocks, hipStream_t s) {
+hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blocks, int threads, hipStream_t s) {
     // The path is chosen once for the launch: every segment's pointers must
     // allow it.
     uintptr_t bits = 0;
@@ -244,13 +244,13 @@ hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blo
     const bool vec16 = (bits & 15) == 0, vec8 = (bits & 7) == 0;
     const int path = sync == FO_SYNC_COHERENT ? (vec8 ? kPathCoherent8 : kPathElem)
                                               : (vec16 ? kPathVec16 : kPathElem);
-    const int64_t per_block = path == kPathCoherent8 ? (int64_t)kThreads * 2 * kUnroll * 4
-                              : path == kPathVec16   ? (int64_t)kThreads * kUnroll * 8
-                                                     : (int64_t)kThreads;
+    const int64_t per_block = path == kPathCoherent8 ? (int64_t)threads * 2 * kUnroll * 4
+                              : path == kPathVec16   ? (int64_t)threads * kUnroll * 8
+                                                     : (int64_t)threads;
     int64_t blocks = (total + per_block - 1) / per_block;
     if (blocks < 1) blocks = 1;
     if (blocks > max_blocks) blocks = max_blocks;
-    const dim3 g((unsigned)blocks), b(kThreads);
+    const dim3 g((unsigned)blocks), b((unsigned)threads);
     if (a.counter) {
         hipLaunchKernelGGL(wait_kernel, dim3(1), dim3(64), 0, s, a.counter, a.target, a.status, a.timeout_ticks);
         const hipError_t e = hipGetLastError();

@@ -36,14 +36,22 @@ int env_mode(const char* name, int dflt) {
 }
 std::atomic<int> g_sync_producer{env_mode("FO_SYNC_PRODUCER", FO_SYNC_COHERENT)};
 std::atomic<int> g_sync_consumer{env_mode("FO_SYNC_CONSUMER", FO_SYNC_COHERENT)};
-std::atomic<int> g_consumer_blocks{[] {
-    const char* e = std::getenv("FO_CONSUMER_BLOCKS");
+int env_int(const char* name, int lo, int hi, int dflt) {
+    const char* e = std::getenv(name);
     if (e && *e) {
         char* end = nullptr;
         const long v = std::strtol(e, &end, 10);
-        if (end && *end == '\0' && v >= 1 && v <= kMaxConsumeBlocks) return (int)v;
+        if (end && *end == '\0' && v >= lo && v <= hi) return (int)v;
     }
-    return kMaxConsumeBlocks;
+    return dflt;
+}
+bool valid_threads(long t) { return t == 64 || t == 128 || t == 256; }
+// Grid of the consumers that run beside the GEMM (default: the full grid,
+// one 256-thread workgroup per compute unit).
+std::atomic<int> g_consumer_blocks{env_int("FO_CONSUMER_BLOCKS", 1, kMaxConsumeBlocks, kMaxConsumeBlocks)};
+std::atomic<int> g_consumer_threads{[] {
+    const int t = env_int("FO_CONSUMER_THREADS", 64, 256, 256);
+    return valid_threads(t) ? t : 256;
 }()};
 
 constexpr int kMaxDevices = 64;
@@ -147,15 +155,20 @@ void fo_get_sync_mode(int32_t* producer, int32_t* consumer) {
     if (consumer) *consumer = fo::g_sync_consumer.load();
 }
 
-fo_status fo_set_consumer_blocks(int32_t max_blocks) {
+fo_status fo_set_consumer_grid(int32_t max_blocks, int32_t threads) {
     fo::clear_error();
     if (max_blocks < 1 || max_blocks > fo::kMaxConsumeBlocks)
         return fo::fail(FO_ERR_ARG, "max_blocks must be in [1, 256]");
+    if (!fo::valid_threads(threads)) return fo::fail(FO_ERR_ARG, "threads must be 64, 128 or 256");
     fo::g_consumer_blocks.store(max_blocks);
+    fo::g_consumer_threads.store(threads);
     return FO_OK;
 }
 
-int32_t fo_get_consumer_blocks(void) { return fo::g_consumer_blocks.load(); }
+void fo_get_consumer_grid(int32_t* max_blocks, int32_t* threads) {
+    if (max_blocks) *max_blocks = fo::g_consumer_blocks.load();
+    if (threads) *threads = fo::g_consumer_threads.load();
+}
 
 fo_status fo_device_num_cus(int32_t device, int32_t* num_cus) {
     fo::clear_error();
@@ -241,7 +254,8 @@ fo_status fo_consume_group(const void* src, const void* peer, void* dst, int64_t
     a.nseg = 1;
     a.seg[0] = fo::ConsumeSegment{0, 0, len};
     hipError_t e = fo::launch_consume(dtype, fo::g_sync_consumer.load(std::memory_order_relaxed), a,
-                                      fo::g_consumer_blocks.load(std::memory_order_relaxed), (hipStream_t)stream);
+                                      fo::g_consumer_blocks.load(std::memory_order_relaxed),
+                                      fo::g_consumer_threads.load(std::memory_order_relaxed), (hipStream_t)stream);
     return e == hipSuccess ? FO_OK : fo::hip_fail("consumer launch", e);
 }
 
@@ -352,6 +366,7 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
     const int nseg = (int)(plan->segs.size() / 5);
     const int sync = fo::g_sync_consumer.load(std::memory_order_relaxed);
     const int cap = fo::g_consumer_blocks.load(std::memory_order_relaxed);
+    const int cap_threads = fo::g_consumer_threads.load(std::memory_order_relaxed);
     fo::ConsumeArgs a{};
     for (int i = 0; i < nseg;) {
         const int64_t j = seg[5 * i];
@@ -363,8 +378,10 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
         for (; i < nseg && seg[5 * i] == j && a.nseg < fo::kMaxConsumeSegments; ++i)
             if (seg[5 * i + 4] > 0) a.seg[a.nseg++] = fo::ConsumeSegment{seg[5 * i + 2], seg[5 * i + 3], seg[5 * i + 4]};
         if (a.nseg == 0) continue;
-        const int blocks = j + 1 == plan->P ? fo::kMaxConsumeBlocks : cap;
-        if ((e = fo::launch_consume(plan->dtype, sync, a, blocks, overlap ? s2 : s1)) != hipSuccess)
+        const bool last = j + 1 == plan->P || !overlap;
+        const int blocks = last ? fo::kMaxConsumeBlocks : cap;
+        const int threads = last ? 256 : cap_threads;
+        if ((e = fo::launch_consume(plan->dtype, sync, a, blocks, threads, overlap ? s2 : s1)) != hipSuccess)
             return fo::hip_fail("consumer launch", e);
     }
     if (overlap) {

@@ -213,19 +213,19 @@ def test_sync_modes(producer, consumer, name):
         fo.set_sync_mode(*old)
 
 
-@pytest.mark.parametrize("blocks", [1, 3, 64])
+@pytest.mark.parametrize("grid", [(1, 64), (3, 256), (64, 128), (256, 64)])
 @pytest.mark.parametrize("name", ["ar_2048x4096x4096", "rs_8192x8192x3584", "a2a_4096x7168x2048"])
-def test_consumer_grid_cap(blocks, name):
-    # a capped consumer grid (grid-stride over every piece of the group)
-    # gives the same bits as the full grid
-    old = fo.get_consumer_blocks()
-    fo.set_consumer_blocks(blocks)
+def test_consumer_grid(grid, name):
+    # any consumer grid (grid-stride over every piece of the group) gives the
+    # same bits
+    old = fo.get_consumer_grid()
+    fo.set_consumer_grid(*grid)
     try:
         M, N, K, cus, sizes = SMALL[name]
         w = workloads.WORKLOADS[name].with_shape(M, N, K)
-        say(f"[consumer blocks] blocks={blocks} {w.name}")
+        say(f"[consumer grid] grid={grid} {w.name}")
         inp = workloads.make_inputs(w)
         plan, o = plan_for(w, inp, num_cus=cus, sizes=list(sizes))
         check(w, inp, plan, o)
     finally:
-        fo.set_consumer_blocks(old)
+        fo.set_consumer_grid(*old)

@@ -165,19 +165,19 @@ def test_header_symbols_are_exported():
 
 def test_process_wide_settings_validate_and_round_trip():
     # host-side setters only: no device work
-    old_modes, old_blocks = fo.get_sync_mode(), fo.get_consumer_blocks()
+    old_modes, old_grid = fo.get_sync_mode(), fo.get_consumer_grid()
     try:
-        for bad in (0, 257, -3):
+        for bad in ((0, 64), (257, 64), (-3, 64), (16, 32), (16, 96), (16, 512)):
             with pytest.raises(fo.FoError) as e:
-                fo.set_consumer_blocks(bad)
+                fo.set_consumer_grid(*bad)
             assert e.value.status == -1
-        assert fo.get_consumer_blocks() == old_blocks
-        fo.set_consumer_blocks(7)
-        assert fo.get_consumer_blocks() == 7
+        assert fo.get_consumer_grid() == old_grid
+        fo.set_consumer_grid(7, 128)
+        assert fo.get_consumer_grid() == (7, 128)
         with pytest.raises(fo.FoError):
             fo.set_sync_mode(3, 0)
         fo.set_sync_mode(1, 0)
         assert fo.get_sync_mode() == (1, 0)
     finally:
-        fo.set_consumer_blocks(old_blocks)
+        fo.set_consumer_grid(*old_grid)
         fo.set_sync_mode(*old_modes)
