@@ -178,6 +178,16 @@ def timed_steps(torch, w, plan, dp, b, s1, s2, steps, warmup):
     return step_us, float(np.mean(gemm)), float(np.median(gemm)), wall
 
 
+def traffic_bytes(w):
+    """HBM bytes per GEMM launch (FETCH_SIZE + WRITE_SIZE, scaled by a plain
+    copy of known size) from the committed rocprofv3 summary of this
+    workload's overlapped steps; None if there is none or the GEMM has
+    changed since it was taken."""
+    from paper_2504_19519_amd import profsum
+    t = profsum.read_traffic(os.path.join(ROOT, "profiles", f"gemm_step_{w.name}.md"), w.name)
+    return None if t is None else round(t)
+
+
 def with_grid(grid, fn):
     """Run fn() with the consumer grid set to `grid` (blocks, threads)."""
     old = fo.get_consumer_grid()
@@ -406,7 +416,8 @@ def main():
                    "pattern": w.pattern, "num_dest": w.num_dest, "waves": T,
                    "groups": [int(x) for x in plan.sizes], "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": round(PEAK_TFLOPS, 1),
-                     "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_TFLOPS, 4), "traffic": None},
+                     "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_TFLOPS, 4),
+                     "traffic": traffic_bytes(w)},
         "gemm": {"signaled_overlapped_us": round(gemm_mean_us, 2), "signaled_overlapped_median_us": round(gemm_med_us, 2),
                  "signaled_alone_us": round(sig_us, 2), "plain_alone_us": round(plain_us, 2),
                  "plain_tflops": round(flops / plain_us / 1e6, 2),
