@@ -32,6 +32,8 @@ namespace fo {
 namespace {
 
 constexpr int kMaxThreads = 256;
+// buffer resource word 3 for raw byte-addressed loads on gfx9
+constexpr int kRsrcWord3 = 0x00020000;
 constexpr int kUnroll = 4;
 
 // The wait of a launch runs in a kernel of its own, one workgroup of one
@@ -188,6 +190,49 @@ __device__ __forceinline__ void stream_coherent8(const uint16_t* __restrict__ sr
     }
 }
 
+// Stream one segment with device-coherent 16-byte source loads (COHERENT;
+// src, peer and dst 16-byte aligned, len * 2 < 2^31): buffer loads with the
+// sc1 cache policy, which a relaxed agent-scope atomic load also uses, so
+// the data the GEMM wrote through to memory is read past this chiplet's L2.
+template <int DT, bool SUM>
+__device__ __forceinline__ void stream_coherent16(const uint16_t* __restrict__ src,
+                                                  const uint16_t* __restrict__ peer,
+                                                  uint16_t* __restrict__ dst, int64_t len) {
+    constexpr int kSc1 = 16;   // cache policy operand: sc1
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)src, 0, (int)(len * 2), kRsrcWord3);
+    const int64_t n16 = len >> 3;
+    const u32x4_t* q = reinterpret_cast<const u32x4_t*>(peer);
+    u32x4_t* d = reinterpret_cast<u32x4_t*>(dst);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (; i + (kUnroll - 1) * stride < n16; i += kUnroll * stride) {
+        u32x4_t x[kUnroll], y[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            x[u] = bit_cast<u32x4_t>(__builtin_amdgcn_raw_buffer_load_b128(rs, (int)((i + u * stride) * 16), 0, kSc1));
+        if constexpr (SUM) {
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) y[u] = __builtin_nontemporal_load(q + i + u * stride);
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) x[u] = add8<DT>(x[u], y[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) __builtin_nontemporal_store(x[u], d + i + u * stride);
+    }
+    for (; i < n16; i += stride) {
+        u32x4_t x = bit_cast<u32x4_t>(__builtin_amdgcn_raw_buffer_load_b128(rs, (int)(i * 16), 0, kSc1));
+        if constexpr (SUM) x = add8<DT>(x, __builtin_nontemporal_load(q + i));
+        __builtin_nontemporal_store(x, d + i);
+    }
+    // ragged tail (< 8 elements): an acquire, then plain 2-byte loads
+    if (blockIdx.x == 0 && threadIdx.x < (len & 7)) {
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        const int64_t e = (n16 << 3) + threadIdx.x;
+        dst[e] = SUM ? add1<DT>(src[e], peer[e]) : src[e];
+    }
+}
+
 // Stream one segment element by element (unaligned buffers).
 template <int DT, bool SUM>
 __device__ __forceinline__ void stream_elem(const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer,
@@ -197,11 +242,12 @@ __device__ __forceinline__ void stream_elem(const uint16_t* __restrict__ src, co
         dst[i] = SUM ? add1<DT>(src[i], peer[i]) : src[i];
 }
 
-enum { kPathVec16 = 0, kPathCoherent8 = 1, kPathElem = 2 };
+enum { kPathVec16 = 0, kPathCoherent8 = 1, kPathElem = 2, kPathCoherent16 = 3 };
 
 // SYNC: how the group is published to the workgroup (check_counter).
-// PATH: kPathCoherent8 goes with SYNC == COHERENT; kPathElem (unaligned
-// buffers) waits with FENCE_ALL in every mode, since plain loads follow.
+// PATH: kPathCoherent16 / kPathCoherent8 go with SYNC == COHERENT;
+// kPathElem (unaligned buffers) waits with FENCE_ALL in every mode, since
+// plain loads follow.
 template <int DT, bool SUM, int SYNC, int PATH>
 __global__ __launch_bounds__(kMaxThreads) void consume_kernel(const ConsumeArgs a) {
     if (a.counter && !check_counter<SYNC>(a.counter, a.target, a.status)) return;
@@ -211,6 +257,7 @@ __global__ __launch_bounds__(kMaxThreads) void consume_kernel(const ConsumeArgs 
         const uint16_t* peer = SUM ? a.peer + g.src_off : nullptr;
         uint16_t* dst = a.dst + g.dst_off;
         if constexpr (PATH == kPathVec16) stream_vec16<DT, SUM>(src, peer, dst, g.len);
+        else if constexpr (PATH == kPathCoherent16) stream_coherent16<DT, SUM>(src, peer, dst, g.len);
         else if constexpr (PATH == kPathCoherent8) stream_coherent8<DT, SUM>(src, peer, dst, g.len);
         else stream_elem<DT, SUM>(src, peer, dst, g.len);
     }
@@ -218,7 +265,9 @@ __global__ __launch_bounds__(kMaxThreads) void consume_kernel(const ConsumeArgs 
 
 template <int DT, bool SUM>
 void launch_variant(int sync, int path, dim3 g, dim3 b, hipStream_t s, const ConsumeArgs& a) {
-    if (path == kPathCoherent8)
+    if (path == kPathCoherent16)
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent16>), g, b, 0, s, a);
+    else if (path == kPathCoherent8)
         hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent8>), g, b, 0, s, a);
     else if (path == kPathVec16 && sync == FO_SYNC_FENCE_ALL)
         hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ALL, kPathVec16>), g, b, 0, s, a);
@@ -234,19 +283,23 @@ hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blo
     // The path is chosen once for the launch: every segment's pointers must
     // allow it.
     uintptr_t bits = 0;
-    int64_t total = 0;
+    int64_t total = 0, longest = 0;
     for (int k = 0; k < a.nseg; ++k) {
         bits |= reinterpret_cast<uintptr_t>(a.src + a.seg[k].src_off) |
                 reinterpret_cast<uintptr_t>(a.dst + a.seg[k].dst_off);
         if (a.peer) bits |= reinterpret_cast<uintptr_t>(a.peer + a.seg[k].src_off);
         total += a.seg[k].len;
+        longest = a.seg[k].len > longest ? a.seg[k].len : longest;
     }
     const bool vec16 = (bits & 15) == 0, vec8 = (bits & 7) == 0;
-    const int path = sync == FO_SYNC_COHERENT ? (vec8 ? kPathCoherent8 : kPathElem)
-                                              : (vec16 ? kPathVec16 : kPathElem);
+    // the 16-byte coherent path addresses a segment with 32-bit byte offsets
+    const bool fits32 = longest * 2 <= 0x7FFFFFFF;
+    const int path = sync == FO_SYNC_COHERENT
+                         ? (vec16 && fits32 ? kPathCoherent16 : vec8 ? kPathCoherent8 : kPathElem)
+                         : (vec16 ? kPathVec16 : kPathElem);
     const int64_t per_block = path == kPathCoherent8 ? (int64_t)threads * 2 * kUnroll * 4
-                              : path == kPathVec16   ? (int64_t)threads * kUnroll * 8
-                                                     : (int64_t)threads;
+                              : path == kPathVec16 || path == kPathCoherent16 ? (int64_t)threads * kUnroll * 8
+                                                                               : (int64_t)threads;
     int64_t blocks = (total + per_block - 1) / per_block;
     if (blocks < 1) blocks = 1;
     if (blocks > max_blocks) blocks = max_blocks;

@@ -280,6 +280,12 @@ fo_status fo_post_reorder(const fo_plan* plan, const void* dev_plan, const void*
     a.gamma = static_cast<const uint16_t*>(gamma);
     a.M = plan->M; a.N = plan->N;
     a.tile_m = plan->tile_m; a.tile_n = plan->tile_n; a.tiles_n = plan->tiles_n;
+    {
+        const int cpt = plan->tile_n / 8;
+        a.cpt_log2 = -1;
+        for (int l = 0; l < 31; ++l)
+            if ((1 << l) == cpt) a.cpt_log2 = l;
+    }
     a.pattern = plan->pattern; a.num_dest = plan->num_dest;
     a.per_dest = plan->pattern == FO_PATTERN_SUBTILE
                      ? (int64_t)plan->tiles * (plan->tile_m / plan->num_dest) * plan->tile_n : 0;
