@@ -7,7 +7,7 @@ consumers on stream 2 -> post-reorder (fused bias / RMSNorm when the workload
 has them). Inputs are resident in HBM before the timed region starts.
 
 Default workload: fp16 GEMM M=8192, N=8192, K=3584 (MLP down-projection
-shard), 256x128 tiles (8 waves on 256 CUs), ReduceScatter stand-in (R=4)
+shard), 256x256 tiles (4 waves on 256 CUs), ReduceScatter stand-in (R=4)
 with the group partition chosen by the planner's predictive search from the
 measured GEMM time and consumer latency curve.
 

@@ -77,8 +77,8 @@ typedef enum {
  *               num_xcds when 0), l = p / num_xcds,
  *               q = x < full ? x*per + l : full*per + (x-full)*(per-1) + l,
  *             then GROUPED on q. On MI355X (8 chiplets of 32 CUs, each with
- *             its own L2) and group_m = 4 a chiplet's 32 concurrent 256x128
- *             tiles form a 4x8 block: 1024 rows of A, 1024 columns of B. */
+ *             its own L2) and group_m = 4 a chiplet's 32 concurrent 256x256
+ *             tiles form a 4x8 block: 1024 rows of A, 2048 columns of B. */
 typedef enum { FO_ORDER_ROWMAJOR = 0, FO_ORDER_GROUPED = 1, FO_ORDER_XCD = 2 } fo_order;
 
 /* Unit of a wave-group partition (Section 3.2 Insight: a group is >= 1 whole

@@ -1,13 +1,14 @@
 // GEMM with the reordering, signalling epilogue (gfx950).
 //
 // C = A x B (Section 2.1.1) with A [M, K] and W = B^T [N, K], both K
-// contiguous. One workgroup computes one BM x BN output tile; workgroup p
-// takes the tile at dispatch position p (fo_order), so tiles run in waves of
-// one tile per compute unit (Section 2.1.1) and position p is the tile's slot
-// in the reordered output (Section 3.3 Approach (1)).
+// contiguous. The grid is persistent: one workgroup per compute unit, each
+// computing BM x BN output tiles one after another. Tiles are taken by
+// dispatch position p (fo_order) in increasing order, so they run in waves
+// of one tile per compute unit (Section 2.1.1) and position p is the tile's
+// slot in the reordered output (Section 3.3 Approach (1)).
 //
 // Main loop: MFMA v_mfma_f32_32x32x16 (fp16 / bf16 in, fp32 accumulate) on
-// k steps of 64, four waves in a 2 x 2 arrangement. A and W tiles move from
+// k steps of 64, 4 or 8 waves of 128 x 64 (or 32 x 32) each. A and W tiles move from
 // memory straight into an LDS ring of STAGES stages (direct global-to-LDS
 // loads, XOR-swizzled rows for conflict-free 16-byte fragment reads), issued
 // STAGES steps ahead; fragments of the next 16-wide k step are read while the
