@@ -31,7 +31,10 @@ struct ConsumeArgs {
 
 // One launch: wait once for *counter >= target, then stream every segment.
 // max_blocks caps the grid (1 .. kMaxConsumeBlocks); threads per workgroup:
-// 64, 128 or 256.
-hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blocks, int threads, hipStream_t s);
+// 64, 128 or 256. full: the launch has the device to itself (more accesses
+// in flight per thread); otherwise it runs beside the GEMM and keeps its
+// registers within what a SIMD running two GEMM waves has left.
+hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blocks, int threads, bool full,
+                          hipStream_t s);
 
 }  // namespace fo

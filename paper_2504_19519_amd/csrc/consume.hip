@@ -34,7 +34,12 @@ namespace {
 constexpr int kMaxThreads = 256;
 // buffer resource word 3 for raw byte-addressed loads on gfx9
 constexpr int kRsrcWord3 = 0x00020000;
-constexpr int kUnroll = 4;
+// Accesses in flight per thread and stream: kUnrollFull for launches that
+// have the device to themselves (the last group of an overlapped run, a
+// serialized run), kUnrollBeside for launches beside the GEMM, whose
+// registers must leave room for the GEMM's waves on the same SIMD.
+constexpr int kUnrollFull = 4;
+constexpr int kUnrollBeside = 2;
 
 // The wait of a launch runs in a kernel of its own, one workgroup of one
 // wave, ahead of the streaming kernel on the same stream: one lane polls the
@@ -108,7 +113,7 @@ __device__ __forceinline__ uint16_t add1(uint16_t x, uint16_t y) {
 
 // Stream one segment, 16 bytes per lane per access (FENCE_ALL / FENCE_ONE;
 // src, peer and dst 16-byte aligned): nontemporal loads and stores.
-template <int DT, bool SUM>
+template <int DT, bool SUM, int kUnroll>
 __device__ __forceinline__ void stream_vec16(const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer,
                                              uint16_t* __restrict__ dst, int64_t len) {
     const int64_t n16 = len >> 3;
@@ -145,7 +150,7 @@ __device__ __forceinline__ void stream_vec16(const uint16_t* __restrict__ src, c
 // Stream one segment with device-coherent 8-byte source loads (COHERENT;
 // src, peer and dst 8-byte aligned). Two 8-byte units per lane per
 // unrolled step.
-template <int DT, bool SUM>
+template <int DT, bool SUM, int kUnroll>
 __device__ __forceinline__ void stream_coherent8(const uint16_t* __restrict__ src,
                                                  const uint16_t* __restrict__ peer,
                                                  uint16_t* __restrict__ dst, int64_t len) {
@@ -194,7 +199,7 @@ __device__ __forceinline__ void stream_coherent8(const uint16_t* __restrict__ sr
 // src, peer and dst 16-byte aligned, len * 2 < 2^31): buffer loads with the
 // sc1 cache policy, which a relaxed agent-scope atomic load also uses, so
 // the data the GEMM wrote through to memory is read past this chiplet's L2.
-template <int DT, bool SUM>
+template <int DT, bool SUM, int kUnroll>
 __device__ __forceinline__ void stream_coherent16(const uint16_t* __restrict__ src,
                                                   const uint16_t* __restrict__ peer,
                                                   uint16_t* __restrict__ dst, int64_t len) {
@@ -248,7 +253,7 @@ enum { kPathVec16 = 0, kPathCoherent8 = 1, kPathElem = 2, kPathCoherent16 = 3 };
 // PATH: kPathCoherent16 / kPathCoherent8 go with SYNC == COHERENT;
 // kPathElem (unaligned buffers) waits with FENCE_ALL in every mode, since
 // plain loads follow.
-template <int DT, bool SUM, int SYNC, int PATH>
+template <int DT, bool SUM, int SYNC, int PATH, int U>
 __global__ __launch_bounds__(kMaxThreads) void consume_kernel(const ConsumeArgs a) {
     if (a.counter && !check_counter<SYNC>(a.counter, a.target, a.status)) return;
     for (int k = 0; k < a.nseg; ++k) {
@@ -256,30 +261,37 @@ __global__ __launch_bounds__(kMaxThreads) void consume_kernel(const ConsumeArgs 
         const uint16_t* src = a.src + g.src_off;
         const uint16_t* peer = SUM ? a.peer + g.src_off : nullptr;
         uint16_t* dst = a.dst + g.dst_off;
-        if constexpr (PATH == kPathVec16) stream_vec16<DT, SUM>(src, peer, dst, g.len);
-        else if constexpr (PATH == kPathCoherent16) stream_coherent16<DT, SUM>(src, peer, dst, g.len);
-        else if constexpr (PATH == kPathCoherent8) stream_coherent8<DT, SUM>(src, peer, dst, g.len);
+        if constexpr (PATH == kPathVec16) stream_vec16<DT, SUM, U>(src, peer, dst, g.len);
+        else if constexpr (PATH == kPathCoherent16) stream_coherent16<DT, SUM, U>(src, peer, dst, g.len);
+        else if constexpr (PATH == kPathCoherent8) stream_coherent8<DT, SUM, U>(src, peer, dst, g.len);
         else stream_elem<DT, SUM>(src, peer, dst, g.len);
     }
 }
 
-template <int DT, bool SUM>
+template <int DT, bool SUM, int U>
 void launch_variant(int sync, int path, dim3 g, dim3 b, hipStream_t s, const ConsumeArgs& a) {
     if (path == kPathCoherent16)
-        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent16>), g, b, 0, s, a);
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent16, U>), g, b, 0, s, a);
     else if (path == kPathCoherent8)
-        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent8>), g, b, 0, s, a);
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent8, U>), g, b, 0, s, a);
     else if (path == kPathVec16 && sync == FO_SYNC_FENCE_ALL)
-        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ALL, kPathVec16>), g, b, 0, s, a);
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ALL, kPathVec16, U>), g, b, 0, s, a);
     else if (path == kPathVec16)
-        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ONE, kPathVec16>), g, b, 0, s, a);
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ONE, kPathVec16, U>), g, b, 0, s, a);
     else
-        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ALL, kPathElem>), g, b, 0, s, a);
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ALL, kPathElem, U>), g, b, 0, s, a);
+}
+
+template <int DT, bool SUM>
+void launch_unroll(bool full, int sync, int path, dim3 g, dim3 b, hipStream_t s, const ConsumeArgs& a) {
+    if (full) launch_variant<DT, SUM, kUnrollFull>(sync, path, g, b, s, a);
+    else launch_variant<DT, SUM, kUnrollBeside>(sync, path, g, b, s, a);
 }
 
 }  // namespace
 
-hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blocks, int threads, hipStream_t s) {
+hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blocks, int threads, bool full,
+                          hipStream_t s) {
     // The path is chosen once for the launch: every segment's pointers must
     // allow it.
     uintptr_t bits = 0;
@@ -297,8 +309,9 @@ hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blo
     const int path = sync == FO_SYNC_COHERENT
                          ? (vec16 && fits32 ? kPathCoherent16 : vec8 ? kPathCoherent8 : kPathElem)
                          : (vec16 ? kPathVec16 : kPathElem);
-    const int64_t per_block = path == kPathCoherent8 ? (int64_t)threads * 2 * kUnroll * 4
-                              : path == kPathVec16 || path == kPathCoherent16 ? (int64_t)threads * kUnroll * 8
+    const int unroll = full ? kUnrollFull : kUnrollBeside;
+    const int64_t per_block = path == kPathCoherent8 ? (int64_t)threads * 2 * unroll * 4
+                              : path == kPathVec16 || path == kPathCoherent16 ? (int64_t)threads * unroll * 8
                                                                                : (int64_t)threads;
     int64_t blocks = (total + per_block - 1) / per_block;
     if (blocks < 1) blocks = 1;
@@ -311,11 +324,11 @@ hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blo
     }
     const bool sum = a.peer != nullptr;
     if (dtype == FO_FP16) {
-        if (sum) launch_variant<FO_FP16, true>(sync, path, g, b, s, a);
-        else launch_variant<FO_FP16, false>(sync, path, g, b, s, a);
+        if (sum) launch_unroll<FO_FP16, true>(full, sync, path, g, b, s, a);
+        else launch_unroll<FO_FP16, false>(full, sync, path, g, b, s, a);
     } else {
-        if (sum) launch_variant<FO_BF16, true>(sync, path, g, b, s, a);
-        else launch_variant<FO_BF16, false>(sync, path, g, b, s, a);
+        if (sum) launch_unroll<FO_BF16, true>(full, sync, path, g, b, s, a);
+        else launch_unroll<FO_BF16, false>(full, sync, path, g, b, s, a);
     }
     return hipGetLastError();
 }

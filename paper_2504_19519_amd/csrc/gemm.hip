@@ -35,7 +35,6 @@
 namespace fo {
 namespace {
 
-constexpr int kBK = 64;             // k values per main-loop step (128 bytes of fp16)
 // s_waitcnt operand for vmcnt = vm and lgkmcnt = lgkm, expcnt at its maximum
 // (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[5:4] at 15:14)
 constexpr int wait_imm(int vm, int lgkm) {
@@ -55,21 +54,29 @@ __device__ __forceinline__ f32x16_t mfma32(u32x4_t a, u32x4_t b, f32x16_t c) {
         return __builtin_amdgcn_mfma_f32_32x32x16_bf16(bit_cast<bf16x8_t>(a), bit_cast<bf16x8_t>(b), c, 0, 0, 0);
 }
 
-// LDS plan of one workgroup. An operand tile row holds the 64 k values of
-// one row of A (or of W) = 128 bytes = 8 chunks of 16 bytes; chunk c of row
-// r is stored at slot c ^ ((r / 2) % 8). The gfx950 LDS serves a 16-byte
-// read for 16 lanes per cycle across 64 banks (256 bytes): rows r and r+1
-// share a 256-byte bank line, so the 16 rows read together at one k position
-// must land in 16 different (row parity, slot) pairs, which this swizzle
-// gives for any 16 consecutive rows.
-template <int BM, int BN, int STAGES, int NW>
+// LDS plan of one workgroup. An operand tile row holds the BK k values of
+// one row of A (or of W): BK * 2 bytes = BK / 8 chunks of 16 bytes; chunk c
+// of row r is stored at slot c ^ ((r >> kSwz) % (BK / 8)). The gfx950 LDS
+// serves a 16-byte read for 16 lanes per cycle across 64 banks (256 bytes):
+// 256 / (BK * 2) consecutive rows share a 256-byte bank line, so the 16 rows
+// read together at one k position must land in 16 different (row within the
+// line, slot) pairs, which this swizzle gives for any 16 consecutive rows
+// (BK = 64: pairs of rows, shift 1; BK = 32: quads of rows, shift 2).
+template <int BM, int BN, int STAGES, int NW, int BK>
 struct Tiles {
-    static constexpr int kRow = kBK * 2;
+    static constexpr int kBK = BK;                       // k values per main-loop step
+    static constexpr int kRow = BK * 2;                  // bytes per operand row
+    static constexpr int kCh = BK / 8;                   // 16-byte chunks per row
+    static constexpr int kSwz = BK == 64 ? 1 : 2;        // log2(rows per bank line)
+    static constexpr int kRowsPerBlk = 1024 / kRow;      // rows per 1 KB load block
     static constexpr int kA = BM * kRow, kB = BN * kRow;
     static constexpr int kStage = kA + kB;
     static constexpr int kLDC = BN + 8;                  // staging row (halfs)
-    // rows staged at once: the whole tile, or half of it, in two stages
-    static constexpr int kRowsPerPass = BM * kLDC * 2 <= 2 * kStage ? BM : BM / 2;
+    // output staging reuses the operand stages: kRowsPerStage staging rows per
+    // stage, a pass stages as many tile rows as fit
+    static constexpr int kRowsPerStage = kStage / (kLDC * 2);
+    static constexpr int kCap = STAGES * kRowsPerStage;
+    static constexpr int kRowsPerPass = BM <= kCap ? BM : BM / 2 <= kCap ? BM / 2 : BM / 4;
     static constexpr int kPasses = BM / kRowsPerPass;
     static constexpr int kAI = kA / 1024 / NW;           // 1 KB load blocks per wave
     static constexpr int kBI = kB / 1024 / NW;
@@ -91,13 +98,18 @@ __device__ __forceinline__ void issue_tile(const uint16_t* Ablk, const uint16_t*
         __builtin_amdgcn_make_buffer_rsrc((void*)Ablk, 0, (int)a_bytes, kRsrcWord3);
     const __amdgpu_buffer_rsrc_t rW =
         __builtin_amdgcn_make_buffer_rsrc((void*)Wblk, 0, (int)w_bytes, kRsrcWord3);
+    // The LDS block addresses (one scalar register each, M0 of the load) are
+    // formed here from an opaque copy of the wave index, so that they are
+    // not all kept live through the main loop.
+    int w = wave;
+    asm volatile("" : "+s"(w));
 #pragma unroll
     for (int i = 0; i < AI; ++i)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void_t*)(st + (wave * AI + i) * 1024), 16, voffA[i],
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void_t*)(st + (w * AI + i) * 1024), 16, voffA[i],
                                                  soff, 0, 0);
 #pragma unroll
     for (int i = 0; i < BI; ++i)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rW, (lds_void_t*)(st + KA + (wave * BI + i) * 1024), 16,
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rW, (lds_void_t*)(st + KA + (w * BI + i) * 1024), 16,
                                                  voffB[i], soff, 0, 0);
 }
 
@@ -132,26 +144,30 @@ __device__ __forceinline__ void wait_and_barrier() {
     asm volatile("" ::: "memory");
 }
 
-template <int DT, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES>
+template <int DT, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int BK>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(const GemmArgs a) {
     constexpr int NW = WAVES_M * WAVES_N, NT = 64 * NW;
     constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
     constexpr int MI = WTM / 32, NJ = WTN / 32;
-    using T = Tiles<BM, BN, STAGES, NW>;
+    using T = Tiles<BM, BN, STAGES, NW, BK>;
+    constexpr int kBK = T::kBK;
+    constexpr int P = kBK / 16;                          // MFMA k steps per main-loop step
     static_assert(NW == 4 || NW == 8, "four or eight waves");
     static_assert(NT >= BM, "one thread per tile row in the epilogue set-up");
     static_assert(WTM % 32 == 0 && WTN % 32 == 0, "32x32 MFMA blocks");
-    static_assert(STAGES == 2 || STAGES == 3, "two or three LDS stages");
+    static_assert(STAGES >= 2 && STAGES <= 4, "two to four LDS stages");
+    static_assert(BK == 32 || BK == 64, "k steps of 32 or 64");
     static_assert(T::kAI >= 1 && T::kBI >= 1 && T::kA % (1024 * NW) == 0 && T::kB % (1024 * NW) == 0,
                   "each wave loads whole 1 KB blocks");
-    static_assert(T::kRowsPerPass * T::kLDC * 2 <= 2 * T::kStage, "output staging fits in two stages");
+    static_assert(T::kRowsPerPass <= T::kCap, "output staging fits in the stages");
     static_assert(T::kRowsPerPass % WTM == 0, "a staging pass holds whole wave rows");
 
     // The stages live in separate arrays, so that the compiler can tell the
     // stage being read from the stages being filled.
     __shared__ __attribute__((aligned(1024))) char st0[T::kStage];
     __shared__ __attribute__((aligned(1024))) char st1[T::kStage];
-    __shared__ __attribute__((aligned(1024))) char st2[STAGES == 3 ? T::kStage : 1024];
+    __shared__ __attribute__((aligned(STAGES >= 3 ? 1024 : 16))) char st2[STAGES >= 3 ? T::kStage : 16];
+    __shared__ __attribute__((aligned(STAGES >= 4 ? 1024 : 16))) char st3[STAGES >= 4 ? T::kStage : 16];
     __shared__ int64_t row_off[BM];
     __shared__ int s_pos;
 
@@ -174,6 +190,11 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
         return cls + D * (int)__hip_atomic_fetch_add(a.dispenser + cls, 1u, __ATOMIC_RELAXED,
                                                      __HIP_MEMORY_SCOPE_AGENT);
     };
+    const bool coherent = a.counters && a.sync == FO_SYNC_COHERENT;
+    auto signal = [&](int group) {
+        if (tid == 0)
+            __hip_atomic_fetch_add(a.counters + group, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    };
     int p = (int)blockIdx.x;
     if (a.dispenser) {
         if (tid == 0) s_pos = claim();
@@ -181,12 +202,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
         p = __builtin_amdgcn_readfirstlane(s_pos);   // uniform: scalar registers
     }
 
-    // A load instruction fills one 1 KB block = 8 rows: lane l writes slot
-    // l % 8 of row r = 8 * block + l / 8, so it fetches chunk
-    // (l % 8) ^ ((r / 2) % 8) of that row.
+    // A load instruction fills one 1 KB block of kRowsPerBlk rows: lane l
+    // writes slot l % kCh of row r = kRowsPerBlk * block + l / kCh, so it
+    // fetches chunk (l % kCh) ^ ((r >> kSwz) % kCh) of that row.
     auto voff = [&](int blk) -> uint32_t {
-        const int r = blk * 8 + (lane >> 3);
-        return (uint32_t)(r * K * 2) + 16u * (uint32_t)((lane & 7) ^ ((r >> 1) & 7));
+        const int r = blk * T::kRowsPerBlk + lane / T::kCh;
+        return (uint32_t)(r * K * 2) +
+               16u * (uint32_t)((lane % T::kCh) ^ ((r >> T::kSwz) & (T::kCh - 1)));
     };
     uint32_t voffA[T::kAI], voffB[T::kBI];
 #pragma unroll
@@ -209,12 +231,15 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
     f32x16_t acc[MI][NJ];
 
     // Fragment addressing: lane l feeds row (l % 32) of a 32-row block with
-    // the 8 consecutive k values of chunk 2*kk + l/32 of the 16-wide step kk.
+    // the 8 consecutive k values of chunk 2*kk + l/32 of the 16-wide step kk
+    // (32-row blocks start on multiples of 32, so the row's swizzle depends
+    // on l only).
     const int a_row = (wm * WTM + (lane & 31)) * T::kRow;
     const int b_row = T::kA + (wn * WTN + (lane & 31)) * T::kRow;
-    int cslot[kBK / 16];
+    int cslot[P];
 #pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) cslot[kk] = 16 * ((2 * kk + (lane >> 5)) ^ ((lane >> 1) & 7));
+    for (int kk = 0; kk < P; ++kk)
+        cslot[kk] = 16 * ((2 * kk + (lane >> 5)) ^ ((lane >> T::kSwz) & (T::kCh - 1)));
 
     // Two fragment register sets: the fragments of k step kk+1 are read from
     // LDS while the MFMAs of k step kk run.
@@ -249,14 +274,16 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
         mma(fa0, fb0);
         interleave_phase<kMfma, kReads, 0>();
         __builtin_amdgcn_sched_barrier(0);
-        load_frags(cur, 2, fa0, fb0);
-        mma(fa1, fb1);
-        interleave_phase<kMfma, kReads, 0>();
-        __builtin_amdgcn_sched_barrier(0);
-        load_frags(cur, 3, fa1, fb1);
-        mma(fa0, fb0);
-        interleave_phase<kMfma, kReads, 0>();
-        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (P == 4) {
+            load_frags(cur, 2, fa0, fb0);
+            mma(fa1, fb1);
+            interleave_phase<kMfma, kReads, 0>();
+            __builtin_amdgcn_sched_barrier(0);
+            load_frags(cur, 3, fa1, fb1);
+            mma(fa0, fb0);
+            interleave_phase<kMfma, kReads, 0>();
+            __builtin_amdgcn_sched_barrier(0);
+        }
         wait_and_barrier<(STAGES - 2) * T::kLoads>();
         issue(kt + STAGES, cur);
         load_frags(nxt, 0, fa0, fb0);
@@ -265,14 +292,14 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
         __builtin_amdgcn_sched_barrier(0);
     };
 
-    // Staging row r of an output pass ([0, kRowsPerPass)): the first half of
-    // the rows in stage 0, the second half in stage 1.
-    constexpr int kHalf = T::kRowsPerPass / 2;
+    // Staging row r of an output pass ([0, kRowsPerPass)): row r % RPS of
+    // stage r / RPS, RPS = kRowsPerStage.
     auto crow = [&](int r) -> uint16_t* {
-        return reinterpret_cast<uint16_t*>(r < kHalf ? st0 + r * T::kLDC * 2 : st1 + (r - kHalf) * T::kLDC * 2);
+        constexpr int RPS = T::kRowsPerStage;
+        const int si = r / RPS, rr = r - (r / RPS) * RPS;
+        char* base = si == 0 ? st0 : si == 1 ? st1 : si == 2 ? st2 : st3;
+        return reinterpret_cast<uint16_t*>(base + rr * T::kLDC * 2);
     };
-    const bool coherent = a.counters && a.sync == FO_SYNC_COHERENT;
-
     while (p < tiles) {
         const int tile = tile_of_position(p, a.tiles_m, a.tiles_n, a.order, a.group_m, a.num_xcds);
         const int tm = tile / a.tiles_n, tn = tile - (tile / a.tiles_n) * a.tiles_n;
@@ -296,11 +323,22 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
 
         issue(0, st0);
         issue(1, st1);
-        if constexpr (STAGES == 3) issue(2, st2);
+        if constexpr (STAGES >= 3) issue(2, st2);
+        if constexpr (STAGES >= 4) issue(3, st3);
         wait_and_barrier<(STAGES - 1) * T::kLoads>();
         load_frags(st0, 0, fa0, fb0);
         int kt = 0;
-        if constexpr (STAGES == 3) {
+        if constexpr (STAGES == 4) {
+            for (; kt + 4 <= KT; kt += 4) {      // tile t lives in stage t % 4
+                step(kt, st0, st1);
+                step(kt + 1, st1, st2);
+                step(kt + 2, st2, st3);
+                step(kt + 3, st3, st0);
+            }
+            if (kt < KT) step(kt, st0, st1);
+            if (kt + 1 < KT) step(kt + 1, st1, st2);
+            if (kt + 2 < KT) step(kt + 2, st2, st3);
+        } else if constexpr (STAGES == 3) {
             for (; kt + 3 <= KT; kt += 3) {      // tile t lives in stage t % 3
                 step(kt, st0, st1);
                 step(kt + 1, st1, st2);
@@ -308,8 +346,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
             }
             if (kt < KT) step(kt, st0, st1);
             if (kt + 1 < KT) step(kt + 1, st1, st2);
-        } else {
-            for (; kt + 2 <= KT; kt += 2) {      // tile t lives in stage t % 2
+        } else {                                 // tile t lives in stage t % 2
+            for (; kt + 2 <= KT; kt += 2) {
                 step(kt, st0, st1);
                 step(kt + 1, st1, st0);
             }
@@ -415,9 +453,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
                 // each wave waits until its write-through stores are complete
                 __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
                 __syncthreads();
-                if (tid == 0)
-                    __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
+                signal(a.slot_group[slot]);
             } else if (a.sync == FO_SYNC_FENCE_ALL) {
                 // every wave: release fence at agent scope (L2 write-back + wait)
                 __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
@@ -445,9 +481,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
     }
 }
 
-template <int DT, int BM, int BN, int WM, int WN, int ST>
+template <int DT, int BM, int BN, int WM, int WN, int ST, int BK>
 hipError_t launch_t(const GemmArgs& a, int grid, hipStream_t s) {
-    hipLaunchKernelGGL((gemm_signal_kernel<DT, BM, BN, WM, WN, ST>), dim3(grid), dim3(64 * WM * WN), 0, s, a);
+    hipLaunchKernelGGL((gemm_signal_kernel<DT, BM, BN, WM, WN, ST, BK>), dim3(grid), dim3(64 * WM * WN), 0, s, a);
     return hipGetLastError();
 }
 
@@ -455,14 +491,14 @@ hipError_t launch_t(const GemmArgs& a, int grid, hipStream_t s) {
 
 hipError_t launch_gemm(int dtype, int tile_m, int tile_n, const GemmArgs& a, int grid, hipStream_t s) {
     if (tile_m == 256 && tile_n == 128)
-        return dtype == FO_FP16 ? launch_t<FO_FP16, 256, 128, 2, 2, 3>(a, grid, s)
-                                : launch_t<FO_BF16, 256, 128, 2, 2, 3>(a, grid, s);
+        return dtype == FO_FP16 ? launch_t<FO_FP16, 256, 128, 2, 2, 3, 64>(a, grid, s)
+                                : launch_t<FO_BF16, 256, 128, 2, 2, 3, 64>(a, grid, s);
     if (tile_m == 256 && tile_n == 256)
-        return dtype == FO_FP16 ? launch_t<FO_FP16, 256, 256, 2, 4, 2>(a, grid, s)
-                                : launch_t<FO_BF16, 256, 256, 2, 4, 2>(a, grid, s);
+        return dtype == FO_FP16 ? launch_t<FO_FP16, 256, 256, 2, 4, 2, 64>(a, grid, s)
+                                : launch_t<FO_BF16, 256, 256, 2, 4, 2, 64>(a, grid, s);
     if (tile_m == 64 && tile_n == 64)
-        return dtype == FO_FP16 ? launch_t<FO_FP16, 64, 64, 2, 2, 3>(a, grid, s)
-                                : launch_t<FO_BF16, 64, 64, 2, 2, 3>(a, grid, s);
+        return dtype == FO_FP16 ? launch_t<FO_FP16, 64, 64, 2, 2, 3, 64>(a, grid, s)
+                                : launch_t<FO_BF16, 64, 64, 2, 2, 3, 64>(a, grid, s);
     return hipErrorInvalidValue;
 }
 

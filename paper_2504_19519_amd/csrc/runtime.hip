@@ -255,7 +255,8 @@ fo_status fo_consume_group(const void* src, const void* peer, void* dst, int64_t
     a.seg[0] = fo::ConsumeSegment{0, 0, len};
     hipError_t e = fo::launch_consume(dtype, fo::g_sync_consumer.load(std::memory_order_relaxed), a,
                                       fo::g_consumer_blocks.load(std::memory_order_relaxed),
-                                      fo::g_consumer_threads.load(std::memory_order_relaxed), (hipStream_t)stream);
+                                      fo::g_consumer_threads.load(std::memory_order_relaxed), false,
+                                      (hipStream_t)stream);
     return e == hipSuccess ? FO_OK : fo::hip_fail("consumer launch", e);
 }
 
@@ -387,7 +388,7 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
         const bool last = j + 1 == plan->P || !overlap;
         const int blocks = last ? fo::kMaxConsumeBlocks : cap;
         const int threads = last ? 256 : cap_threads;
-        if ((e = fo::launch_consume(plan->dtype, sync, a, blocks, threads, overlap ? s2 : s1)) != hipSuccess)
+        if ((e = fo::launch_consume(plan->dtype, sync, a, blocks, threads, last, overlap ? s2 : s1)) != hipSuccess)
             return fo::hip_fail("consumer launch", e);
     }
     if (overlap) {
