@@ -52,8 +52,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="rs_8192x8192x3584", choices=list(workloads.WORKLOADS))
-    ap.add_argument("--phase", default="all", choices=["all", "step", "gemm", "copy"],
-                    help="step/gemm/copy run only that loop (for profiler runs)")
+    ap.add_argument("--phase", default="all", choices=["all", "step", "gemm", "copy", "predict"],
+                    help="step/gemm/copy run only that loop (for profiler runs); predict: Algorithm 1's "
+                         "estimate vs the measured GEMM+consume time of every partition")
     ap.add_argument("--sizes", default=None, help="explicit partition in waves, e.g. 1,1,2,4")
     ap.add_argument("--tile", default=None, help="override the workload's output tile, e.g. 256x256")
     ap.add_argument("--consumer-grid", default=None,
@@ -137,6 +138,9 @@ def make_plan(w, inp, num_cus, sizes=None, pattern=None, gemm_us=0.0, curve=None
               dest_perm=inp.sigma if pattern == "subtile" else None,
               row_bucket=inp.bucket if pattern == "subtoken" else None)
     if sizes is not None:
+        if curve is not None:      # given partition + Algorithm 1's estimate of it
+            return fo.plan_groups(w.M, w.N, w.K, sizes=list(sizes), gemm_us=gemm_us, curve_bytes=curve[0],
+                                  curve_us=curve[1], **kw)
         return fo.plan_groups(w.M, w.N, w.K, sizes=list(sizes), **kw)
     if curve is None:
         tiles = (w.M // w.tile_m) * (w.N // w.tile_n)
@@ -215,6 +219,77 @@ def consumer_curve(torch, w, b, stream, total_elems):
     return xs, ys
 
 
+def gemm_comm_times(torch, w, plan, dp, b, s1, s2, steps):
+    """GEMM + consume time of overlapped runs: from the GEMM's start (event
+    on the GEMM stream) to the end of the last consumer (event on the
+    communication stream); the post-reorder is not included."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    dummy = torch.cuda.Event(enable_timing=True)
+    dummy.record(s1)
+    for a, c in ev:          # create the events
+        a.record(s1)
+        c.record(s2)
+    for a, c in ev:
+        run_step(torch, w, plan, dp, b, s1, s2, (a, dummy))
+        c.record(s2)
+    torch.cuda.synchronize()
+    if int(b.status.cpu()[0]) != 0:
+        raise RuntimeError("a consumer wait timed out")
+    return [a.elapsed_time(c) * 1000.0 for a, c in ev]
+
+
+def partitions(T):
+    """Every composition of T waves, by cut vector (bit i = cut after wave i+1)."""
+    out = []
+    for x in range(1 << (T - 1)):
+        sizes, run = [], 0
+        for wv in range(1, T + 1):
+            run += 1
+            if wv == T or (x >> (wv - 1)) & 1:
+                sizes.append(run)
+                run = 0
+        out.append(tuple(sizes))
+    return out
+
+
+def predictor_accuracy(torch, w, inp, b, base_plan, dp_base, num_cus, T, flops, s1, s2, args):
+    """Algorithm 1's estimate against the measured GEMM+consume time for every
+    partition of the waves (interleaved rounds), and the searched partition's
+    measured time against the best measured one."""
+    log("predictor: GEMM alone and consumer curve")
+    sig_us = time_gemm(torch, base_plan, dp_base, b, s1, 50, 10)
+    xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N)
+    cands = partitions(T)
+    plans = {}
+    for c in cands:
+        p = make_plan(w, inp, num_cus, sizes=c, gemm_us=sig_us, curve=(xs, ys))
+        plans[c] = (p, dev_plan(torch, p))
+    searched = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys))
+    torch.cuda.synchronize()
+    meas = {c: [] for c in cands}
+    for c in cands:                      # warm-up
+        gemm_comm_times(torch, w, plans[c][0], plans[c][1], b, s1, s2, 2)
+    for _ in range(5):
+        for c in cands:
+            meas[c] += gemm_comm_times(torch, w, plans[c][0], plans[c][1], b, s1, s2, 4)
+    rows = []
+    for c in cands:
+        m = float(np.median(meas[c]))
+        pr = plans[c][0].predicted_us
+        rows.append({"groups": list(c), "predicted_us": round(pr, 2), "measured_us": round(m, 2),
+                     "error_pct": round((pr - m) / m * 100, 2)})
+    best = min(rows, key=lambda r: r["measured_us"])
+    pick = next(r for r in rows if tuple(r["groups"]) == tuple(int(x) for x in searched.sizes))
+    pred_best = min(rows, key=lambda r: r["predicted_us"])
+    return {"phase": "predict", "workload": w.name, "waves": T, "gemm_alone_us": round(sig_us, 2),
+            "mean_abs_error_pct": round(float(np.mean([abs(r["error_pct"]) for r in rows])), 2),
+            "searched_groups": pick["groups"], "searched_measured_us": pick["measured_us"],
+            "best_measured_groups": best["groups"], "best_measured_us": best["measured_us"],
+            "searched_over_best": round(best["measured_us"] / pick["measured_us"], 4),
+            "unpruned_predicted_best": pred_best["groups"], "partitions": rows}
+
+
 def cpu_baseline(w, inp, seconds):
     import oracle
     threads = oracle.num_threads()
@@ -278,6 +353,10 @@ def main():
             args.steps, args.warmup, s1))
         print(json.dumps({"phase": "copy", "bytes_read": 2 * n, "bytes_written": 2 * n, "us": us}))
         return
+    if args.phase == "predict":
+        print(json.dumps(predictor_accuracy(torch, w, inp, b, base_plan, dp_base, num_cus, T, flops, s1, s2,
+                                            args)), flush=True)
+        return
     if args.phase == "gemm":
         us = time_gemm(torch, base_plan, dp_base, b, s1, args.steps, args.warmup)
         print(json.dumps({"phase": "gemm", "us": us, "tflops": flops / us / 1e6}))
@@ -324,13 +403,12 @@ def main():
     log(f"plan: T={plan.T} groups={list(plan.sizes)} predicted {plan.predicted_us:.1f} us")
 
     # ---- timed steps -----------------------------------------------------
-    log(f"timed steps: warmup {args.warmup}, steps {args.steps}")
-    step_us, gemm_mean_us, gemm_med_us, wall = timed_steps(torch, w, plan, dp, b, s1, s2, args.steps,
-                                                           args.warmup)
     # overlapped vs serialized, in alternating rounds so that both see the
     # same device state (clock, temperature)
+    log("overlapped vs serialized rounds")
     rounds, per = 5, max(4, args.steps // 5)
-    ov, se, ov_g, se_g = [], [], [], []
+    ov, se, ov_g, se_g, gc, ga, ca = [], [], [], [], [], [], []
+    n_all = w.M * w.N
     for _ in range(rounds):
         us, gm, _, _ = timed_steps(torch, w, plan, dp, b, s1, s2, per, 2)
         ov.append(us)
@@ -338,7 +416,23 @@ def main():
         us, gm, _, _ = timed_steps(torch, w, plan, dp, b, s1, s1, per, 2)
         se.append(us)
         se_g.append(gm)
+        # GEMM + consume of the overlapped run, the GEMM alone and the
+        # consumer alone (whole buffer, full grid), in the same round
+        gc.append(float(np.median(gemm_comm_times(torch, w, plan, dp, b, s1, s2, per))))
+        ga.append(time_gemm(torch, base_plan, dp_base, b, s1, per, 1))
+        ca.append(with_grid((256, 256), lambda: time_loop(
+            torch, lambda: fo.consume_group(b.C, b.peer, b.dst, n_all, w.dtype, None, 0, None, s1), per, 1, s1)))
     ov_us, serial_us = float(np.median(ov)), float(np.median(se))
+    gc_us, ga_us, ca_us = float(np.median(gc)), float(np.median(ga)), float(np.median(ca))
+
+    # the timed region: exactly `steps` overlapped steps after `warmup` ones
+    log(f"timed steps: warmup {args.warmup}, steps {args.steps}")
+    step_us, gemm_mean_us, gemm_med_us, wall = timed_steps(torch, w, plan, dp, b, s1, s2, args.steps,
+                                                           args.warmup)
+
+    # ---- Algorithm 1's estimate vs measurement, every partition ------------
+    pred = predictor_accuracy(torch, w, inp, b, base_plan, dp_base, num_cus, T, flops, s1, s2, args) \
+        if 1 < T <= 8 else None
 
     # ---- group-size sweep (waves per group) ---------------------------------
     sweep = {}
@@ -450,13 +544,15 @@ def main():
                     "gemm_in_overlapped_us": round(float(np.median(ov_g)), 2),
                     "gemm_in_serial_us": round(float(np.median(se_g)), 2),
                     "speedup_vs_serial": round(serial_us / ov_us, 4),
-                    "overlapped_gemm_consume_over_max": round(
-                        (ov_us - post_us) / max(sig_us, cons_all_us), 4),
+                    "gemm_consume_overlapped_us": round(gc_us, 2),
+                    "gemm_alone_us": round(ga_us, 2), "consume_alone_us": round(ca_us, 2),
+                    "overlapped_gemm_consume_over_max": round(gc_us / max(ga_us, ca_us), 4),
                     "theoretical_bound_us": round(bound_us + post_us, 2),
                     "predicted_us": round(plan.predicted_us, 2),
                     "paper_context": "up to 1.65x overlap speedup on 4x RTX 4090 over PCIe (multi-GPU "
                                      "collectives; not comparable to this 1-GPU stand-in)"},
         "sweep_waves_per_group": sweep,
+        "predictor": None if pred is None else {k: v for k, v in pred.items() if k != "phase"},
         "sync_modes": {"default": list(default_modes), "variants": sync_variants,
                        "overlapped_equals_serial_bits": consistent},
         "consumer_grid": {"default": "%dx%d" % default_grid, "variants": grid_variants},

@@ -109,10 +109,13 @@ typedef struct {
     int32_t num_groups;       /* > 0: explicit `sizes`; 0: Algorithm 1 search       */
     const int32_t* sizes;     /* [num_groups], each >= 1, summing to T waves (or to
                                  the tile count when unit == TILES)                 */
-    double gemm_us;           /* search: measured GEMM duration                     */
-    const double* curve_bytes;/* search: sampled communication latency curve,      */
-    const double* curve_us;   /*   ascending bytes; piecewise-linear in between,    */
-    int32_t curve_len;        /*   end-point bandwidth outside the samples          */
+    double gemm_us;           /* search (or estimate of given waves): measured GEMM
+                                 duration                                          */
+    const double* curve_bytes;/* sampled communication latency curve (required by  */
+    const double* curve_us;   /*   the search; optional with given waves, then the  */
+    int32_t curve_len;        /*   plan carries their estimate): ascending bytes,
+                                 piecewise-linear in between, end-point bandwidth
+                                 outside the samples                               */
     int32_t s_first, s_last;  /* search pruning |G_1| <= s_first, |G_P| <= s_last
                                  (Section 4.1 uses 2 and 4); <= 0 means no bound    */
 } fo_grouping;
@@ -157,8 +160,10 @@ const int32_t* fo_plan_order(const fo_plan* plan);         /* [tiles] position -
 const int32_t* fo_plan_tile_to_slot(const fo_plan* plan);  /* [tiles] the reorder map  */
 const int32_t* fo_plan_group_first(const fo_plan* plan);   /* [P+1] first slot          */
 const int32_t* fo_plan_group_targets(const fo_plan* plan); /* [P] tiles = final count   */
-double fo_plan_predicted_us(const fo_plan* plan);     /* Algorithm 1 estimate (0 if
-                                                         the partition was given)   */
+double fo_plan_predicted_us(const fo_plan* plan);     /* Algorithm 1 estimate of the
+                                                         plan's partition (searched,
+                                                         or given in waves with a
+                                                         curve); else 0             */
 /* SUBTOKEN pools: pool_base[(s * B) + b] = subtokens of pool b in slots < s,
  * s in [0, tiles]; pool_off[b] = first subtoken of pool b, b in [0, B]. */
 const int32_t* fo_plan_pool_base(const fo_plan* plan);

@@ -76,6 +76,16 @@ double predict(const fo_plan& p, const std::vector<int32_t>& sizes, double gemm_
     return std::max(acc_p, acc_m) + comm(sizes.size() - 1);
 }
 
+fo_status check_curve(const fo_grouping& g) {
+    for (int i = 0; i < g.curve_len; ++i) {
+        if (!(g.curve_bytes[i] > 0.0) || !(g.curve_us[i] >= 0.0) ||
+            (i > 0 && !(g.curve_bytes[i] > g.curve_bytes[i - 1])))
+            return fo::fail(FO_ERR_ARG, "curve bytes must be positive and ascending, latencies >= 0");
+    }
+    if (!(g.gemm_us >= 0.0)) return fo::fail(FO_ERR_ARG, "gemm_us must be >= 0");
+    return FO_OK;
+}
+
 fo_status search(fo_plan& p, const fo_grouping& g) {
     if (p.T == 0) return FO_OK;
     if (p.T > kMaxSearchWaves)
@@ -233,17 +243,21 @@ fo_status build(fo_plan& p, const fo_problem& pr, const fo_grouping& g) {
         const int64_t want = g.unit == FO_UNIT_WAVES ? p.T : p.tiles;
         if (sum != want) return fo::fail(FO_ERR_ARG, "group sizes must sum to the number of waves (or tiles)");
         p.sizes.assign(g.sizes, g.sizes + g.num_groups);
+        // With a latency curve, the given partition gets Algorithm 1's
+        // estimate too (no search).
+        if (g.unit == FO_UNIT_WAVES && p.T > 0 && g.curve_len >= 1 && g.curve_bytes && g.curve_us) {
+            fo_status st = check_curve(g);
+            if (st != FO_OK) return st;
+            std::vector<int32_t> first;
+            p.predicted_us = predict(p, p.sizes, g.gemm_us, g, first);
+        }
     } else {
         if (g.unit != FO_UNIT_WAVES) return fo::fail(FO_ERR_ARG, "the search partitions waves");
         if (p.T > 0) {
             if (g.curve_len < 1 || !g.curve_bytes || !g.curve_us)
                 return fo::fail(FO_ERR_ARG, "the search needs a latency curve");
-            for (int i = 0; i < g.curve_len; ++i) {
-                if (!(g.curve_bytes[i] > 0.0) || !(g.curve_us[i] >= 0.0) ||
-                    (i > 0 && !(g.curve_bytes[i] > g.curve_bytes[i - 1])))
-                    return fo::fail(FO_ERR_ARG, "curve bytes must be positive and ascending, latencies >= 0");
-            }
-            if (!(g.gemm_us >= 0.0)) return fo::fail(FO_ERR_ARG, "gemm_us must be >= 0");
+            fo_status st = check_curve(g);
+            if (st != FO_OK) return st;
         }
         fo_status st = search(p, g);
         if (st != FO_OK) return st;

@@ -181,3 +181,34 @@ def test_process_wide_settings_validate_and_round_trip():
     finally:
         fo.set_consumer_grid(*old_grid)
         fo.set_sync_mode(*old_modes)
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("pattern,nd", [("tile", 0), ("subtoken", 8), ("subtile", 4)])
+def test_given_partition_estimate_matches_oracle(seed, pattern, nd):
+    # a partition given in waves together with a curve carries Algorithm 1's
+    # estimate of that partition: the oracle's latency recurrence on it
+    rng = np.random.default_rng(200 + seed)
+    M, N, BM, BN = 4096, 7168, 256, 128      # 896 tiles
+    cus = int(rng.choice([64, 128, 256]))
+    xs, ys = _curve(seed + 10)
+    gemm_us = float(rng.uniform(20, 400))
+    T = -(-896 // cus)
+    cuts = sorted(rng.choice(np.arange(1, T), size=int(rng.integers(0, T)), replace=False)) if T > 1 else []
+    sizes = tuple(int(b - a) for a, b in zip([0] + list(cuts), list(cuts) + [T]))
+    bucket = rng.integers(0, nd, M) if pattern == "subtoken" else None
+    sigma = rng.permutation(nd) if pattern == "subtile" else None
+    p = fo.plan_groups(M, N, 2048, num_cus=cus, pattern=pattern, num_dest=nd, row_bucket=bucket,
+                       dest_perm=sigma, sizes=list(sizes), gemm_us=gemm_us, curve_bytes=xs, curve_us=ys)
+    o = oracle.make_plan(M, N, BM, BN, num_cus=cus, order="xcd", pattern=pattern, num_dest=nd,
+                         bucket=bucket, sigma=sigma, sizes=sizes)
+    first = oracle.group_first_slots(sizes, "waves", o.W, o.tiles)
+    lat = [oracle.interp_latency(xs, ys, oracle.slot_range_bytes(o, first[j], first[j + 1], 2))
+           for j in range(len(sizes))]
+    t = oracle.predicted_latency(sizes, T, gemm_us, lambda j: lat[j])
+    assert tuple(p.sizes) == sizes
+    assert p.predicted_us == pytest.approx(t, rel=1e-12)
+    # without a curve there is no estimate
+    q = fo.plan_groups(M, N, 2048, num_cus=cus, pattern=pattern, num_dest=nd, row_bucket=bucket,
+                       dest_perm=sigma, sizes=list(sizes))
+    assert q.predicted_us == 0.0
