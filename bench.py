@@ -52,7 +52,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="rs_8192x8192x3584", choices=list(workloads.WORKLOADS))
-    ap.add_argument("--phase", default="all", choices=["all", "step", "gemm", "copy", "predict"],
+    ap.add_argument("--phase", default="all", choices=["all", "step", "gemm", "copy", "predict", "trace"],
                     help="step/gemm/copy run only that loop (for profiler runs); predict: Algorithm 1's "
                          "estimate vs the measured GEMM+consume time of every partition")
     ap.add_argument("--sizes", default=None, help="explicit partition in waves, e.g. 1,1,2,4")
@@ -290,6 +290,49 @@ def predictor_accuracy(torch, w, inp, b, base_plan, dp_base, num_cus, T, flops, 
             "unpruned_predicted_best": pred_best["groups"], "partitions": rows}
 
 
+def tile_timeline(torch, w, plan, dp, b, stream):
+    """Wave pattern of the signalling GEMM (Section 2.1.1, Figure 3): one
+    traced launch after warm-up; per wave of W positions, how far apart its
+    tiles start and finish against the wave's length, and whether position p
+    ran on chiplet p mod 8 as the XCD dispatch order assumes."""
+    tiles = plan.tiles
+    trace = torch.zeros(4 * tiles, dtype=torch.int64, device="cuda")
+    time_gemm(torch, plan, dp, b, stream, 10, 5)
+    fo.set_tile_trace(trace, tiles)
+    try:
+        time_gemm(torch, plan, dp, b, stream, 1, 0)
+    finally:
+        fo.set_tile_trace(None)
+    khz = fo.device_wall_clock_khz()
+    t = trace.cpu().numpy().reshape(-1, 4)
+    us = 1000.0 / khz
+    t0 = t[:, 0].min()
+    start, end = (t[:, 0] - t0) * us, (t[:, 1] - t0) * us
+    chip = (t[:, 2] >> 32) & 0xF
+    W, T = plan.W, plan.T
+    waves = []
+    prev_end = 0.0
+    for j in range(T):
+        sl = slice(j * W, min((j + 1) * W, tiles))
+        e_mean = float(end[sl].mean())
+        waves.append({"wave": j, "tiles": int(end[sl].size),
+                      "start_us": [round(float(start[sl].min()), 2), round(float(start[sl].max()), 2)],
+                      "end_us": [round(float(end[sl].min()), 2), round(float(end[sl].max()), 2)],
+                      "end_spread_over_wave_len": round(float(end[sl].max() - end[sl].min()) /
+                                                        max(e_mean - prev_end, 1e-9), 4)})
+        prev_end = e_mean
+    pos = np.arange(tiles)
+    dur = end - start
+    per_chip = [{"chiplet": int(c), "tiles": int((chip == c).sum()),
+                 "mean_tile_us": round(float(dur[chip == c].mean()), 2),
+                 "last_end_us": round(float(end[chip == c].max()), 2)} for c in sorted(set(chip.tolist()))]
+    return {"phase": "trace", "workload": w.name, "tiles": int(tiles), "wave_width": int(W), "waves": waves,
+            "per_chiplet": per_chip,
+            "kernel_us": round(float(end.max()), 2),
+            "chiplets_seen": int(len(set(chip.tolist()))),
+            "position_on_chiplet_p_mod_8": round(float(np.mean(chip == pos % 8)), 4)}
+
+
 def cpu_baseline(w, inp, seconds):
     import oracle
     threads = oracle.num_threads()
@@ -352,6 +395,9 @@ def main():
             torch, lambda: fo.consume_group(b.C, None, b.dst, n, w.dtype, None, 0, None, s1),
             args.steps, args.warmup, s1))
         print(json.dumps({"phase": "copy", "bytes_read": 2 * n, "bytes_written": 2 * n, "us": us}))
+        return
+    if args.phase == "trace":
+        print(json.dumps(tile_timeline(torch, w, base_plan, dp_base, b, s1)), flush=True)
         return
     if args.phase == "predict":
         print(json.dumps(predictor_accuracy(torch, w, inp, b, base_plan, dp_base, num_cus, T, flops, s1, s2,

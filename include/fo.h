@@ -349,6 +349,19 @@ void fo_get_consumer_grid(int32_t* max_blocks, int32_t* threads);
 void fo_set_poll_timeout_us(int64_t us);
 int64_t fo_get_poll_timeout_us(void);
 
+/* Tile timeline (the wave pattern of Section 2.1.1, Figure 3). While set,
+ * every fo_gemm_signal_reorder launch writes, for each dispatch position
+ * p < capacity_tiles, four uint64 at trace[4p]: the device wall clock
+ * (s_memrealtime ticks, fo_device_wall_clock_khz) when the tile started, the
+ * wall clock when all of its stores had completed, the chiplet (XCC_ID
+ * register, high 32 bits) and hardware id (HW_ID register, low 32 bits) of
+ * the compute unit that ran it, and the workgroup index. Tracing adds a
+ * store drain and a barrier per tile. trace: caller-owned device memory,
+ * 8-byte aligned; NULL stops tracing. Process-wide. */
+fo_status fo_set_tile_trace(uint64_t* trace, int64_t capacity_tiles);
+/* Ticks per millisecond of the device wall clock of the current device. */
+fo_status fo_device_wall_clock_khz(int32_t* khz);
+
 /* Compute units of HIP device `device` (for fo_problem.num_cus). */
 fo_status fo_device_num_cus(int32_t device, int32_t* num_cus);
 

@@ -21,7 +21,7 @@ __all__ = [
     "FoError", "Plan", "plan_groups", "gemm_signal_reorder", "consume_group",
     "post_reorder", "reset_counters", "run_overlapped", "set_poll_timeout_us",
     "get_poll_timeout_us", "device_num_cus", "set_sync_mode", "get_sync_mode",
-    "set_consumer_grid", "get_consumer_grid", "LIB_PATH",
+    "set_consumer_grid", "get_consumer_grid", "set_tile_trace", "device_wall_clock_khz", "LIB_PATH",
     "FP16", "BF16", "TILE", "SUBTILE", "SUBTOKEN", "ROWMAJOR",
 ]
 
@@ -103,6 +103,8 @@ def lib() -> ctypes.CDLL:
     L.fo_set_sync_mode.argtypes, L.fo_set_sync_mode.restype = [i32, i32], ctypes.c_int
     L.fo_get_sync_mode.argtypes = [pi32, pi32]
     L.fo_set_consumer_grid.argtypes, L.fo_set_consumer_grid.restype = [i32, i32], ctypes.c_int
+    L.fo_set_tile_trace.argtypes, L.fo_set_tile_trace.restype = [vp, i64], ctypes.c_int
+    L.fo_device_wall_clock_khz.argtypes, L.fo_device_wall_clock_khz.restype = [pi32], ctypes.c_int
     L.fo_get_consumer_grid.argtypes = [pi32, pi32]
     L.fo_set_poll_timeout_us.argtypes = [i64]
     L.fo_get_poll_timeout_us.restype = i64
@@ -335,6 +337,18 @@ def get_consumer_grid():
     b, t = ctypes.c_int32(), ctypes.c_int32()
     lib().fo_get_consumer_grid(ctypes.byref(b), ctypes.byref(t))
     return int(b.value), int(t.value)
+
+
+def set_tile_trace(trace, capacity_tiles: int = 0) -> None:
+    """Record the tile timeline of subsequent GEMM launches into `trace`
+    (device buffer of 4 x uint64 per tile); None stops tracing."""
+    _check(lib().fo_set_tile_trace(_ptr(trace), int(capacity_tiles) if trace is not None else 0))
+
+
+def device_wall_clock_khz() -> int:
+    k = ctypes.c_int32()
+    _check(lib().fo_device_wall_clock_khz(ctypes.byref(k)))
+    return int(k.value)
 
 
 def set_poll_timeout_us(us: int) -> None:

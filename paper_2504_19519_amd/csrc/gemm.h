@@ -25,6 +25,8 @@ struct GemmArgs {
     uint32_t* dispenser;           // [num_dispensers] zeroed position counters, or null
     int32_t num_dispensers;        // D >= 1 (with a dispenser)
     int32_t sync;                  // fo_sync_mode of the producer side
+    uint64_t* trace;               // [4 * trace_cap] tile timeline, or null
+    int64_t trace_cap;
 };
 
 // grid: number of persistent workgroups (at most the number of tiles; with

@@ -301,6 +301,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
         return reinterpret_cast<uint16_t*>(base + rr * T::kLDC * 2);
     };
     while (p < tiles) {
+        const uint64_t t_start = a.trace ? wall_clock64() : 0;
         const int tile = tile_of_position(p, a.tiles_m, a.tiles_n, a.order, a.group_m, a.num_xcds);
         const int tm = tile / a.tiles_n, tn = tile - (tile / a.tiles_n) * a.tiles_n;
         Ablk = a.A + (int64_t)tm * BM * K;
@@ -467,6 +468,20 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
                 if (tid == 0)
                     __hip_atomic_fetch_add(a.counters + a.slot_group[slot], 1u, __ATOMIC_RELEASE,
                                            __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        if (a.trace && p < a.trace_cap) {
+            // tile timeline: start, completion of every store of the tile,
+            // chiplet and compute unit (hardware id registers), workgroup
+            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+            __syncthreads();
+            if (tid == 0) {
+                uint64_t* t = a.trace + 4 * (int64_t)p;
+                t[0] = t_start;
+                t[1] = wall_clock64();
+                t[2] = ((uint64_t)__builtin_amdgcn_s_getreg((31 << 11) | 20) << 32) |
+                       (uint32_t)__builtin_amdgcn_s_getreg((31 << 11) | 4);
+                t[3] = blockIdx.x;
             }
         }
         // Every wave is done with the staging tile (the next tile's loads

@@ -54,6 +54,10 @@ std::atomic<int> g_consumer_threads{[] {
     return valid_threads(t) ? t : 256;
 }()};
 
+// Tile timeline buffer of the GEMM launches (fo_set_tile_trace).
+std::atomic<uint64_t*> g_trace{nullptr};
+std::atomic<int64_t> g_trace_cap{0};
+
 constexpr int kMaxDevices = 64;
 std::atomic<int64_t> g_clock_khz[kMaxDevices];   // 0 = unknown
 
@@ -170,6 +174,25 @@ void fo_get_consumer_grid(int32_t* max_blocks, int32_t* threads) {
     if (threads) *threads = fo::g_consumer_threads.load();
 }
 
+fo_status fo_set_tile_trace(uint64_t* trace, int64_t capacity_tiles) {
+    fo::clear_error();
+    if (trace && capacity_tiles < 1) return fo::fail(FO_ERR_ARG, "capacity_tiles must be >= 1");
+    if (trace && (reinterpret_cast<uintptr_t>(trace) & 7)) return fo::fail(FO_ERR_ARG, "trace must be 8-byte aligned");
+    fo::g_trace_cap.store(trace ? capacity_tiles : 0);
+    fo::g_trace.store(trace);
+    return FO_OK;
+}
+
+fo_status fo_device_wall_clock_khz(int32_t* khz) {
+    fo::clear_error();
+    if (!khz) return fo::fail(FO_ERR_ARG, "khz is NULL");
+    int64_t k = 0;
+    fo_status st = fo::clock_khz(&k);
+    if (st != FO_OK) return st;
+    *khz = (int32_t)k;
+    return FO_OK;
+}
+
 fo_status fo_device_num_cus(int32_t device, int32_t* num_cus) {
     fo::clear_error();
     if (!num_cus) return fo::fail(FO_ERR_ARG, "num_cus is NULL");
@@ -227,6 +250,8 @@ fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan, cons
     }
     a.counters = plan->P > 0 ? counters : nullptr;
     a.sync = fo::g_sync_producer.load(std::memory_order_relaxed);
+    a.trace = fo::g_trace.load(std::memory_order_relaxed);
+    a.trace_cap = a.trace ? fo::g_trace_cap.load(std::memory_order_relaxed) : 0;
     // Persistent grid: one workgroup per tile of a wave. Position classes
     // follow the chiplet of the XCD dispatch order.
     const int grid = std::min(plan->tiles, std::max(plan->W, 1));

@@ -224,3 +224,33 @@ def test_bad_arguments_are_rejected_before_launch():
         fo.consume_group(0, None, 0, 10, "fp16")
     with pytest.raises(fo.FoError):
         fo.consume_group(256, None, 256, -1, "fp16")
+
+
+def test_tile_trace():
+    # the tile timeline: one record per dispatch position, start <= end, the
+    # workgroup that ran it within the grid; outputs are unchanged by tracing
+    torch = torch_mod()
+    M, N, K = 1024, 1280, 256
+    say("[tile trace] 1024x1280x256 tiles 256x256")
+    A, W = _operands(M, N, K, "fp16", 21)
+    plan = fo.plan_groups(M, N, K, dtype="fp16", tile_m=256, tile_n=256, order="xcd", num_cus=8,
+                          pattern="tile", sizes=[3])
+    dA, dW = to_dev(A), to_dev(W)
+    dp = dev_plan(plan)
+    ref = empty16(M * N, "fp16")
+    ctr = zeros_u32(plan.num_counters)
+    fo.gemm_signal_reorder(plan, dp, dA, dW, ref, ctr)
+    trace = torch.zeros(4 * plan.tiles, dtype=torch.int64, device="cuda")
+    fo.set_tile_trace(trace, plan.tiles)
+    try:
+        C = empty16(M * N, "fp16")
+        ctr = zeros_u32(plan.num_counters)
+        fo.gemm_signal_reorder(plan, dp, dA, dW, C, ctr)
+        torch.cuda.synchronize()
+    finally:
+        fo.set_tile_trace(None)
+    np.testing.assert_array_equal(from_dev(C)[:M * N], from_dev(ref)[:M * N])
+    t = trace.cpu().numpy().reshape(-1, 4)
+    assert np.all(t[:, 0] > 0) and np.all(t[:, 1] >= t[:, 0])
+    assert np.all((t[:, 3] >= 0) & (t[:, 3] < min(plan.tiles, plan.W)))
+    assert fo.device_wall_clock_khz() > 0
