@@ -28,13 +28,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kRowsPerBlock = kThreads / 64;
 
-struct RowSrc {
-    // source element offset of chunk c (8 elements) of the row
-    int64_t row_part;    // pattern-dependent row offset inside a slot unit
-    int64_t unit;        // elements per slot unit (tile, subtile or 0)
-    int64_t dest_base;   // SUBTILE: destination buffer base
-};
-
 template <int DT>
 __device__ __forceinline__ void widen8(u32x4_t v, float* f) {
 #pragma unroll
