@@ -71,9 +71,13 @@ struct Tiles {
     static constexpr int kRowsPerBlk = 1024 / kRow;      // rows per 1 KB load block
     static constexpr int kA = BM * kRow, kB = BN * kRow;
     static constexpr int kStage = kA + kB;
-    static constexpr int kLDC = BN + 8;                  // staging row (halfs)
-    // output staging reuses the operand stages: kRowsPerStage staging rows per
+    // Output staging reuses the operand stages: a staging row holds BN halfs
+    // (BN / 8 chunks of 16 bytes); chunk c of row r is stored at chunk
+    // c ^ (r % (BN / 8)), so that the 32 rows a half-wave writes at one
+    // column land on different banks. kRowsPerStage staging rows per
     // stage, a pass stages as many tile rows as fit
+    static constexpr int kLDC = BN;                      // staging row (halfs)
+    static constexpr int kCCh = BN / 8;                  // staging chunks per row
     static constexpr int kRowsPerStage = kStage / (kLDC * 2);
     static constexpr int kCap = STAGES * kRowsPerStage;
     static constexpr int kRowsPerPass = BM <= kCap ? BM : BM / 2 <= kCap ? BM / 2 : BM / 4;
@@ -292,13 +296,15 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
         __builtin_amdgcn_sched_barrier(0);
     };
 
-    // Staging row r of an output pass ([0, kRowsPerPass)): row r % RPS of
-    // stage r / RPS, RPS = kRowsPerStage.
-    auto crow = [&](int r) -> uint16_t* {
+    // Column n (a multiple of 4 halfs) of staging row r of an output pass
+    // ([0, kRowsPerPass)): row r % RPS of stage r / RPS, RPS = kRowsPerStage,
+    // chunk (n / 8) ^ (r % kCCh).
+    auto cptr = [&](int r, int n) -> uint16_t* {
         constexpr int RPS = T::kRowsPerStage;
         const int si = r / RPS, rr = r - (r / RPS) * RPS;
         char* base = si == 0 ? st0 : si == 1 ? st1 : si == 2 ? st2 : st3;
-        return reinterpret_cast<uint16_t*>(base + rr * T::kLDC * 2);
+        const int chunk = (n >> 3) ^ (r & (T::kCCh - 1));
+        return reinterpret_cast<uint16_t*>(base + rr * T::kLDC * 2 + chunk * 16 + (n & 7) * 2);
     };
     while (p < tiles) {
         const uint64_t t_start = a.trace ? wall_clock64() : 0;
@@ -409,7 +415,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
                             u32x2_t v;
                             v[0] = pack2<DT>(acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]);
                             v[1] = pack2<DT>(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-                            *reinterpret_cast<u32x2_t*>(crow(m) + n) = v;
+                            *reinterpret_cast<u32x2_t*>(cptr(m, n)) = v;
                         }
                     }
                 }
@@ -429,7 +435,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
 #pragma unroll
                     for (int cc = 0; cc < CPL; ++cc) {
                         const int col = lc + cc * 64;
-                        const uint64_t v = *reinterpret_cast<const uint64_t*>(crow(r) + col * 4);
+                        const uint64_t v = *reinterpret_cast<const uint64_t*>(cptr(r, col * 4));
                         __hip_atomic_store(reinterpret_cast<uint64_t*>(a.C + row_off[r0 + r]) + col, v,
                                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     }
@@ -440,7 +446,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
                 const int c = tid_e % CPR;
 #pragma unroll 4
                 for (int r = tid_e / CPR; r < T::kRowsPerPass; r += RPP) {
-                    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(crow(r) + c * 8);
+                    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(cptr(r, c * 8));
                     *reinterpret_cast<u32x4_t*>(a.C + row_off[r0 + r] + c * 8) = v;
                 }
             }
