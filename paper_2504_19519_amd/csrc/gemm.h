@@ -25,6 +25,7 @@ struct GemmArgs {
     uint32_t* dispenser;           // [num_dispensers] zeroed position counters, or null
     int32_t num_dispensers;        // D >= 1 (with a dispenser)
     int32_t sync;                  // fo_sync_mode of the producer side
+    int32_t c_rsrc;                // 1: C fits a 31-bit byte range (16-byte buffer stores)
     uint64_t* trace;               // [4 * trace_cap] tile timeline, or null
     int64_t trace_cap;
 };

@@ -43,6 +43,8 @@ constexpr int wait_imm(int vm, int lgkm) {
 constexpr int kWaitVmcnt0 = wait_imm(0, 15);
 // buffer resource word 3 for raw byte-addressed loads on gfx9
 constexpr int kRsrcWord3 = 0x00020000;
+// cache-policy operand of a buffer store: sc1 (device-coherent write-through)
+constexpr int kCachePolicySc1 = 16;
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
@@ -421,10 +423,26 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
                 }
             }
             __syncthreads();
-            if (coherent) {
-                // Device-coherent 8-byte stores (written through to the point
-                // all chiplets share): no cache write-back is needed before
-                // the signal.
+            if (coherent && a.c_rsrc) {
+                // Device-coherent 16-byte stores (cache policy sc1: written
+                // through to the point all chiplets share), addressed through
+                // a buffer resource over C: no cache write-back is needed
+                // before the signal.
+                const __amdgpu_buffer_rsrc_t rC =
+                    __builtin_amdgcn_make_buffer_rsrc((void*)a.C, 0, 0x7FFFFFFF, kRsrcWord3);
+                constexpr int CPR = BN / 8;             // 16-byte chunks per tile row
+                constexpr int RPP = NT / CPR;           // rows per pass of the workgroup
+                const int c = tid_e % CPR;
+#pragma unroll 4
+                for (int r = tid_e / CPR; r < T::kRowsPerPass; r += RPP) {
+                    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(cptr(r, c * 8));
+                    __builtin_amdgcn_raw_buffer_store_b128(v, rC, (uint32_t)((row_off[r0 + r] + c * 8) * 2), 0,
+                                                           kCachePolicySc1);
+                }
+            } else if (coherent) {
+                // Device-coherent 8-byte stores for outputs past a 31-bit
+                // byte range (written through to the point all chiplets
+                // share): no cache write-back is needed before the signal.
                 constexpr int LPR = BN / 4;             // lanes per row (8 bytes each)
                 constexpr int RPI = LPR >= 64 ? 1 : 64 / LPR;   // rows per wave_e instruction
                 constexpr int CPL = LPR >= 64 ? LPR / 64 : 1;   // 8-byte columns per lane_e

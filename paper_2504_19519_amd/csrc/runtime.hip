@@ -250,6 +250,7 @@ fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan, cons
     }
     a.counters = plan->P > 0 ? counters : nullptr;
     a.sync = fo::g_sync_producer.load(std::memory_order_relaxed);
+    a.c_rsrc = plan->M * plan->N * 2 <= INT32_MAX ? 1 : 0;
     a.trace = fo::g_trace.load(std::memory_order_relaxed);
     a.trace_cap = a.trace ? fo::g_trace_cap.load(std::memory_order_relaxed) : 0;
     // Persistent grid: one workgroup per tile of a wave. Position classes
