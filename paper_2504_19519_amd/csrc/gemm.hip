@@ -28,6 +28,8 @@
 //      adds 1 to the counter of the group that owns the slot.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "fo_device.h"
 #include "fo_internal.h"
 #include "gemm.h"
@@ -269,13 +271,21 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
     };
 
     constexpr int kMfma = MI * NJ, kReads = MI + NJ;
+    // Group of the previous tile whose count is still to be sent (or -1):
+    // with device-coherent stores and two stages, a tile's count goes out at
+    // the first main-loop barrier of the workgroup's next tile, so that the
+    // stores complete while the next tile's first loads are in flight.
+    int pend = -1;
+    constexpr std::true_type kYes{};
+    constexpr std::false_type kNo{};
+    const bool defer = STAGES == 2 && coherent && !a.trace;
     // Step kt multiplies the tile in stage `cur` (its k step 0 fragments are
     // already in fa0/fb0; tile kt+1 is in stage `nxt`). Before its last k
     // step, every wave has read all of `cur` and tile kt+1 has landed (tiles
     // up to kt+STAGES-1 may still be loading): after the barrier, tile
     // kt+STAGES goes into `cur`, and the first fragments of tile kt+1 are read
     // while the last MFMAs of tile kt run.
-    auto step = [&](int kt, char* cur, const char* nxt) {
+    auto step = [&](int kt, char* cur, const char* nxt, auto first_c) {
         load_frags(cur, 1, fa1, fb1);
         mma(fa0, fb0);
         interleave_phase<kMfma, kReads, 0>();
@@ -291,6 +301,15 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
             __builtin_amdgcn_sched_barrier(0);
         }
         wait_and_barrier<(STAGES - 2) * T::kLoads>();
+        if constexpr (STAGES == 2 && decltype(first_c)::value) {
+            // The previous tile's stores are complete in every wave (this
+            // barrier follows a vmcnt(0) wait): its deferred count goes out.
+            if (pend >= 0) {
+                if (tid == 0)
+                    __hip_atomic_fetch_add(a.counters + pend, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                pend = -1;
+            }
+        }
         issue(kt + STAGES, cur);
         load_frags(nxt, 0, fa0, fb0);
         mma(fa1, fb1);
@@ -317,6 +336,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
 
         // Plan lookups needed only by the epilogue: issued now, consumed later.
         const int slot = a.tile_to_slot ? a.tile_to_slot[tile] : p;
+        const int group = a.counters ? a.slot_group[slot] : 0;
         int bucket = 0, rank = 0;
         if (a.pattern == FO_PATTERN_SUBTOKEN && tid < BM) {
             bucket = a.row_bucket[tm * BM + tid];
@@ -339,28 +359,30 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
         int kt = 0;
         if constexpr (STAGES == 4) {
             for (; kt + 4 <= KT; kt += 4) {      // tile t lives in stage t % 4
-                step(kt, st0, st1);
-                step(kt + 1, st1, st2);
-                step(kt + 2, st2, st3);
-                step(kt + 3, st3, st0);
+                step(kt, st0, st1, kNo);
+                step(kt + 1, st1, st2, kNo);
+                step(kt + 2, st2, st3, kNo);
+                step(kt + 3, st3, st0, kNo);
             }
-            if (kt < KT) step(kt, st0, st1);
-            if (kt + 1 < KT) step(kt + 1, st1, st2);
-            if (kt + 2 < KT) step(kt + 2, st2, st3);
+            if (kt < KT) step(kt, st0, st1, kNo);
+            if (kt + 1 < KT) step(kt + 1, st1, st2, kNo);
+            if (kt + 2 < KT) step(kt + 2, st2, st3, kNo);
         } else if constexpr (STAGES == 3) {
             for (; kt + 3 <= KT; kt += 3) {      // tile t lives in stage t % 3
-                step(kt, st0, st1);
-                step(kt + 1, st1, st2);
-                step(kt + 2, st2, st0);
+                step(kt, st0, st1, kNo);
+                step(kt + 1, st1, st2, kNo);
+                step(kt + 2, st2, st0, kNo);
             }
-            if (kt < KT) step(kt, st0, st1);
-            if (kt + 1 < KT) step(kt + 1, st1, st2);
+            if (kt < KT) step(kt, st0, st1, kNo);
+            if (kt + 1 < KT) step(kt + 1, st1, st2, kNo);
         } else {                                 // tile t lives in stage t % 2
-            for (; kt + 2 <= KT; kt += 2) {
-                step(kt, st0, st1);
-                step(kt + 1, st1, st0);
+            // the first step sends the previous tile's deferred count
+            step(0, st0, st1, kYes);
+            for (kt = 1; kt + 2 <= KT; kt += 2) {
+                step(kt, st1, st0, kNo);
+                step(kt + 1, st0, st1, kNo);
             }
-            if (kt < KT) step(kt, st0, st1);
+            if (kt < KT) step(kt, st1, st0, kNo);
         }
         wait_and_barrier<0>();    // no load may still be writing LDS
         __syncthreads();          // operand stages are reused for the output tile
@@ -471,14 +493,14 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
             if (pass + 1 < T::kPasses) __syncthreads();   // staging is refilled
         }
 
-        if (a.counters) {
+        if (a.counters && !defer) {
             // Section 3.2: count the finished tile for its group once all of
             // the tile's stores are visible to every compute unit.
             if (coherent) {
                 // each wave waits until its write-through stores are complete
                 __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
                 __syncthreads();
-                signal(a.slot_group[slot]);
+                signal(group);
             } else if (a.sync == FO_SYNC_FENCE_ALL) {
                 // every wave: release fence at agent scope (L2 write-back + wait)
                 __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
@@ -509,14 +531,27 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
             }
         }
         // Every wave is done with the staging tile (the next tile's loads
-        // overwrite it) before the next position is published.
-        __syncthreads();
+        // overwrite it) before the next position is published; the tile's
+        // stores may still be in flight.
+        wait_and_barrier<63>();
         if (a.dispenser) {
             if (tid == 0) s_pos = next;
-            __syncthreads();
+            wait_and_barrier<63>();
             next = s_pos;
         }
         p = __builtin_amdgcn_readfirstlane(next);
+        if (a.counters && defer) {
+            // Section 3.2 as above: this tile's count is sent once all of its
+            // stores are complete -- after the next tile's first main-loop
+            // barrier, or now if this was the workgroup's last tile.
+            if (p < tiles) {
+                pend = group;
+            } else {
+                __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+                __syncthreads();
+                signal(group);
+            }
+        }
     }
 }
 

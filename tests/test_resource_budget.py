@@ -9,6 +9,7 @@ LDS per compute unit; a consumer workgroup has one wave per SIMD).
 """
 import json
 import os
+import re
 
 import pytest
 
@@ -36,8 +37,11 @@ def test_consumer_fits_beside_every_gemm_kernel():
     c_lds = max(v["lds"] for v in cons.values())
     for name, v in gemm.items():
         assert v.get("vgpr_spill", 0) == 0, name
-        # waves of one GEMM workgroup per SIMD: 256 threads -> 1, 512 -> 2
-        per_simd = 2 if ("ILi2ELi4E" in name) else 1
+        # waves of one GEMM workgroup per SIMD (template arguments: dtype,
+        # tile_m, tile_n, waves_m, waves_n, stages, k step): 4 waves -> 1, 8 -> 2
+        m = re.search(r"gemm_signal_kernelILi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)E", name)
+        assert m, name
+        per_simd = (int(m.group(4)) * int(m.group(5)) + 3) // 4
         regs = per_simd * _round8(v["vgpr"] + v.get("agpr", 0))
         assert regs + c_regs <= 512, (name, regs, c_regs)
         assert v["lds"] + c_lds <= 160 * 1024, (name, v["lds"], c_lds)
