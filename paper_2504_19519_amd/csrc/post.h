@@ -13,7 +13,7 @@ struct PostArgs {
     const uint16_t* gamma;      // [N] or null
     int64_t M, N;
     int32_t tile_m, tile_n, tiles_n, pattern, num_dest;
-    int32_t cpt_log2;           // log2(tile_n / 8) if a power of two, else -1
+    int32_t cpt_log2;           // log2(tile_n / 8) (a power of two for reordered patterns)
     int64_t per_dest;           // SUBTILE: elements of one destination buffer
     const int32_t* tile_to_slot;
     const int32_t* dest_perm;
@@ -25,6 +25,9 @@ struct PostArgs {
     int32_t do_norm;
 };
 
+// LDS bytes one post-reorder workgroup uses (source piece offsets of its 4
+// rows; bias and gamma chunks when the row is normalised in registers).
+size_t post_lds_bytes(const PostArgs& a);
 hipError_t launch_post(int dtype, const PostArgs& a, hipStream_t s);
 
 }  // namespace fo

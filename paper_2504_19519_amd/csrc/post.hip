@@ -4,18 +4,26 @@
 //
 // One wave per output row, four rows per workgroup. Lane l handles the
 // 16-byte chunks l, l+64, ... of the row. A chunk lies inside one tile
-// column, so its source address is the row's place in that tile's slot (tile
-// pattern), in the slice's destination buffer (subtile pattern) or in the
-// row's pool (subtoken pattern); every source read is 16 contiguous bytes
-// and lanes of one tile column read one contiguous tile_n-wide row piece.
-// The workgroup first copies the slots of its tile row from the reorder map
-// into LDS, so a chunk's address needs no dependent global load. Loads are
-// issued in batches (16 per lane, or the whole row when it is held for
-// RMSNorm) before their stores, so that many reads are in flight. Output
-// rows are written fully coalesced; source and output bypass the caches
-// (nontemporal). With RMSNorm the row is held in registers between the
-// sum-of-squares pass and the scaling pass (rows up to 8192 wide), or read
-// twice for wider rows.
+// column, so its source is 16 contiguous bytes of one row piece: the row's
+// place in that tile's slot (tile pattern), in the slice's destination
+// buffer (subtile pattern) or in the row's pool (subtoken pattern), and
+// lanes of one tile column read one contiguous tile_n-wide piece.
+//
+// The workgroup first resolves the reorder map for its rows: for every
+// (row, tile column) it writes the offset of the source piece to LDS. After
+// that a chunk's source address is one LDS read and an add, so all of a
+// lane's loads can be in flight at once.
+//
+// Two kernels:
+//   post_gather_kernel  the plain restore (bit-exact copy): 16 loads per lane
+//                       in flight before their stores;
+//   post_norm_kernel    bias add and/or RMSNorm: the row is loaded up front
+//                       and held in registers between the sum-of-squares and
+//                       the scaling (rows up to 8192 wide, bias and gamma
+//                       copied to LDS), or read twice for wider rows.
+// Sources are read through the caches (the consumer has just written them,
+// so part of them is still in the memory-side cache); the output is written
+// nontemporal.
 #include <hip/hip_runtime.h>
 
 #include "fo_device.h"
@@ -27,6 +35,11 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kRowsPerBlock = kThreads / 64;
+constexpr int kMaxRegChunks = 64 * 16;     // rows held in registers: up to 8192 columns
+
+typedef __attribute__((address_space(3))) char lds_char_t;
+typedef __attribute__((address_space(3))) uint32_t lds_u32_t;
+typedef __attribute__((address_space(3))) u32x4_t lds_u32x4_t;
 
 template <int DT>
 __device__ __forceinline__ void widen8(u32x4_t v, float* f) {
@@ -37,159 +50,225 @@ __device__ __forceinline__ void widen8(u32x4_t v, float* f) {
     }
 }
 
-// Slots of one tile row kept in LDS (tile rows up to this many tiles; wider
-// tile rows read the map from memory).
-constexpr int kSlotCache = 1024;
-
-template <int DT, int CH>
-__global__ __launch_bounds__(kThreads, 4) void post_kernel(const PostArgs a) {
-    __shared__ int32_t s_slot[kSlotCache];
-    const int lane = threadIdx.x & 63;
-    const int64_t i0 = (int64_t)blockIdx.x * kRowsPerBlock;
-    const int64_t tm0 = i0 / a.tile_m;
-    const bool cached = a.pattern != FO_PATTERN_ROWMAJOR && a.tiles_n <= kSlotCache;
-    if (cached) {     // uniform over the workgroup
-        for (int t = threadIdx.x; t < a.tiles_n; t += kThreads) s_slot[t] = a.tile_to_slot[tm0 * a.tiles_n + t];
-        __syncthreads();
-    }
-    const int64_t i = i0 + (threadIdx.x >> 6);
-    if (i >= a.M) return;
-    const int64_t nch = a.N >> 3;
-    const int64_t tm = i / a.tile_m;
-    const int64_t r = i - tm * a.tile_m;
-    const int cpt = a.tile_n >> 3;                      // chunks per tile row piece
-
-    // Row-level part of the source address.
-    int64_t row_part = 0, dest_base = 0;
-    int32_t b = 0;
+// Offset, in 16-byte chunks of the consumer's buffer, of the tile_n-wide
+// source piece of output row i in tile column tn.
+__device__ __forceinline__ uint32_t piece_offset(const PostArgs& a, int64_t i, int tn) {
+    const int64_t tw = a.tile_n;
+    if (a.pattern == FO_PATTERN_ROWMAJOR) return (uint32_t)((i * a.N + tn * tw) >> 3);
+    const int32_t tm = (int32_t)(i / a.tile_m);
+    const int32_t r = (int32_t)(i - (int64_t)tm * a.tile_m);
+    const int64_t slot = a.tile_to_slot[(int64_t)tm * a.tiles_n + tn];
+    int64_t off;
     if (a.pattern == FO_PATTERN_TILE) {
-        row_part = r * a.tile_n;
+        off = (slot * a.tile_m + r) * tw;
     } else if (a.pattern == FO_PATTERN_SUBTILE) {
-        const int64_t h = a.tile_m / a.num_dest;
-        const int64_t k = r / h;
-        dest_base = (int64_t)a.dest_perm[k] * a.per_dest;
-        row_part = (r - k * h) * a.tile_n;
-    } else if (a.pattern == FO_PATTERN_SUBTOKEN) {
-        b = a.row_bucket[i];
-        row_part = ((int64_t)a.pool_off[b] + a.row_rank[i]) * a.tile_n;
+        const int32_t h = a.tile_m / a.num_dest;
+        const int32_t k = r / h;
+        off = (int64_t)a.dest_perm[k] * a.per_dest + (slot * h + (r - k * h)) * tw;
+    } else {
+        const int32_t b = a.row_bucket[i];
+        off = ((int64_t)a.pool_off[b] + a.pool_base[slot * a.num_dest + b] + a.row_rank[i]) * tw;
     }
-    const bool from_lds = cached && tm == tm0;
-    auto src_of = [&](int64_t c) -> int64_t {
-        if (a.pattern == FO_PATTERN_ROWMAJOR) return i * a.N + c * 8;
-        const int64_t tn = a.cpt_log2 >= 0 ? c >> a.cpt_log2 : c / cpt;
-        const int64_t cin = (c - tn * cpt) * 8;
-        const int64_t slot = from_lds ? s_slot[tn] : a.tile_to_slot[tm * a.tiles_n + tn];
-        if (a.pattern == FO_PATTERN_TILE) return slot * a.tile_m * a.tile_n + row_part + cin;
-        if (a.pattern == FO_PATTERN_SUBTILE)
-            return dest_base + slot * (a.tile_m / a.num_dest) * a.tile_n + row_part + cin;
-        return row_part + (int64_t)a.pool_base[slot * a.num_dest + b] * a.tile_n + cin;
-    };
-    auto load = [&](int64_t c) -> u32x4_t {
-        return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.src + src_of(c)));
-    };
+    return (uint32_t)(off >> 3);
+}
+
+// Source pieces of the workgroup's rows i0 .. i0+3: bases[w * tiles_n + tn].
+__device__ __forceinline__ void stage_pieces(const PostArgs& a, lds_u32_t* bases, int64_t i0) {
+    const int n = kRowsPerBlock * a.tiles_n;
+    for (int idx = threadIdx.x; idx < n; idx += kThreads) {
+        const int w = idx / a.tiles_n, tn = idx - (idx / a.tiles_n) * a.tiles_n;
+        const int64_t i = i0 + w;
+        if (i < a.M) bases[idx] = piece_offset(a, i, tn);
+    }
+}
+
+// Chunk c of the row whose piece offsets are `bases` (tile_n / 8 is a power
+// of two, 1 << cpt_log2).
+__device__ __forceinline__ u32x4_t load_chunk(const PostArgs& a, const lds_u32_t* bases, int64_t c) {
+    const uint32_t cpt_mask = (1u << a.cpt_log2) - 1u;
+    const uint32_t off = bases[(uint32_t)c >> a.cpt_log2] + ((uint32_t)c & cpt_mask);
+    return reinterpret_cast<const u32x4_t*>(a.src)[off];
+}
+
+template <int DT>
+__global__ __launch_bounds__(kThreads) void post_gather_kernel(const PostArgs a) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    lds_u32_t* bases = reinterpret_cast<lds_u32_t*>((lds_char_t*)smem);
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t i0 = (int64_t)blockIdx.x * kRowsPerBlock;
+    stage_pieces(a, bases, i0);
+    __syncthreads();
+    const int64_t i = i0 + w;
+    if (i >= a.M) return;
+    const lds_u32_t* rb = bases + w * a.tiles_n;
+    const int64_t nch = a.N >> 3;
+    u32x4_t* out4 = reinterpret_cast<u32x4_t*>(a.out + i * a.N);
+    constexpr int B = 16;
+    for (int64_t c0 = lane; c0 < nch; c0 += 64 * B) {
+        u32x4_t v[B];
+#pragma unroll
+        for (int t = 0; t < B; ++t)
+            if (c0 + 64 * t < nch) v[t] = load_chunk(a, rb, c0 + 64 * t);
+#pragma unroll
+        for (int t = 0; t < B; ++t)
+            if (c0 + 64 * t < nch) __builtin_nontemporal_store(v[t], out4 + c0 + 64 * t);
+    }
+}
+
+// y = (x + bias) [* rsqrt(mean((x + bias)^2) + eps) * gamma]: bias and gamma
+// are optional (null pointers), AFFINE says whether either is present.
+template <int DT, int CH, bool AFFINE>
+__global__ __launch_bounds__(kThreads) void post_norm_kernel(const PostArgs a) {
+    constexpr bool kLdsAffine = AFFINE && CH > 0;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int64_t nch = a.N >> 3;
+    // LDS: [bias chunks][gamma chunks] (with kLdsAffine), then the pieces
+    lds_u32x4_t* s_bias = reinterpret_cast<lds_u32x4_t*>((lds_char_t*)smem);
+    lds_u32x4_t* s_gamma = s_bias + (kLdsAffine ? nch : 0);
+    lds_u32_t* bases = reinterpret_cast<lds_u32_t*>(s_gamma + (kLdsAffine ? nch : 0));
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t i0 = (int64_t)blockIdx.x * kRowsPerBlock;
     const u32x4_t* bias4 = reinterpret_cast<const u32x4_t*>(a.bias);
     const u32x4_t* gamma4 = reinterpret_cast<const u32x4_t*>(a.gamma);
+    const bool has_bias = AFFINE && a.bias;
+    const bool has_gamma = AFFINE && a.do_norm && a.gamma;
+    const u32x4_t zero = {0u, 0u, 0u, 0u};
+    if constexpr (kLdsAffine) {
+        for (int64_t c = threadIdx.x; c < nch; c += kThreads) {
+            s_bias[c] = has_bias ? bias4[c] : zero;
+            s_gamma[c] = has_gamma ? gamma4[c] : zero;
+        }
+    }
+    stage_pieces(a, bases, i0);
+    __syncthreads();
+    const int64_t i = i0 + w;
+    if (i >= a.M) return;
+    const lds_u32_t* rb = bases + w * a.tiles_n;
     u32x4_t* out4 = reinterpret_cast<u32x4_t*>(a.out + i * a.N);
+    auto bias_at = [&](int64_t c) -> u32x4_t {
+        if constexpr (kLdsAffine) return s_bias[c];
+        else return has_bias ? bias4[c] : zero;
+    };
+    auto gamma_at = [&](int64_t c) -> u32x4_t {
+        if constexpr (kLdsAffine) return s_gamma[c];
+        else return has_gamma ? gamma4[c] : zero;
+    };
 
-    auto finish = [&](int64_t c, u32x4_t xv, float inv) {
-        float x[8], bv[8], gv[8];
-        widen8<DT>(xv, x);
-        if (a.bias) widen8<DT>(bias4[c], bv);
-        if (a.do_norm && a.gamma) widen8<DT>(gamma4[c], gv);
+    // h = x + bias (fp32, no rounding)
+    auto shift = [&](u32x4_t xv, int64_t c, float* h) {
+        widen8<DT>(xv, h);
+        if (has_bias) {
+            float bv[8];
+            widen8<DT>(bias_at(c), bv);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) h[e] += bv[e];
+        }
+    };
+    auto sumsq = [&](u32x4_t xv, int64_t c) {
+        float h[8];
+        shift(xv, c, h);
+        float s = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s += h[e] * h[e];
+        return s;
+    };
+    auto finish = [&](int64_t c, u32x4_t xv, float inv, bool live) {
+        float h[8], gv[8];
+        shift(xv, c, h);
+        if (has_gamma) widen8<DT>(gamma_at(c), gv);
         u32x4_t o;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            float y0 = x[2 * e] + (a.bias ? bv[2 * e] : 0.0f);
-            float y1 = x[2 * e + 1] + (a.bias ? bv[2 * e + 1] : 0.0f);
+            float y0 = h[2 * e], y1 = h[2 * e + 1];
             if (a.do_norm) {
                 y0 *= inv;
                 y1 *= inv;
-                if (a.gamma) {
+                if (has_gamma) {
                     y0 *= gv[2 * e];
                     y1 *= gv[2 * e + 1];
                 }
             }
             o[e] = pack2<DT>(y0, y1);
         }
-        __builtin_nontemporal_store(o, out4 + c);
+        if (live) __builtin_nontemporal_store(o, out4 + c);
     };
-    auto sumsq = [&](int64_t c, u32x4_t xv) {
-        float x[8], bv[8];
-        widen8<DT>(xv, x);
-        if (a.bias) widen8<DT>(bias4[c], bv);
-        float s = 0.0f;
+    auto rsqrt_mean = [&](float ss) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const float h = x[e] + (a.bias ? bv[e] : 0.0f);
-            s += h * h;
-        }
-        return s;
+        for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
+        return 1.0f / sqrtf(ss / (float)a.N + a.eps);
     };
 
-    if (!a.do_norm && !a.bias) {          // plain gather: bit-exact copy
-        constexpr int B = 16;
-        for (int64_t c0 = lane; c0 < nch; c0 += 64 * B) {
-            u32x4_t v[B];
-#pragma unroll
-            for (int t = 0; t < B; ++t)
-                if (c0 + 64 * t < nch) v[t] = load(c0 + 64 * t);
-#pragma unroll
-            for (int t = 0; t < B; ++t)
-                if (c0 + 64 * t < nch) __builtin_nontemporal_store(v[t], out4 + c0 + 64 * t);
-        }
-        return;
-    }
-    float ss = 0.0f;
     if constexpr (CH > 0) {
-        u32x4_t cache[CH];
+        // The row is loaded up front. Lanes past the row's end load its last
+        // chunk (no branches around the loads: the array stays in registers)
+        // and drop the result.
+        u32x4_t xc[CH];
 #pragma unroll
         for (int t = 0; t < CH; ++t) {
             const int64_t c = lane + 64 * t;
-            if (c < nch) cache[t] = load(c);
-        }
-        if (a.do_norm) {
-#pragma unroll
-            for (int t = 0; t < CH; ++t) {
-                const int64_t c = lane + 64 * t;
-                if (c < nch) ss += sumsq(c, cache[t]);
-            }
+            xc[t] = load_chunk(a, rb, c < nch ? c : nch - 1);
         }
         float inv = 1.0f;
         if (a.do_norm) {
+            float ss = 0.0f;
 #pragma unroll
-            for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
-            inv = 1.0f / sqrtf(ss / (float)a.N + a.eps);
+            for (int t = 0; t < CH; ++t) {
+                const int64_t c = lane + 64 * t;
+                const float q = sumsq(xc[t], c < nch ? c : nch - 1);
+                ss += c < nch ? q : 0.0f;
+                // bias chunks are read from LDS one at a time, not all hoisted
+                if constexpr (kLdsAffine) asm volatile("" ::: "memory");
+            }
+            inv = rsqrt_mean(ss);
         }
+        // The scaling pass widens the stored chunks again instead of keeping
+        // the fp32 row of the first pass alive (twice the registers).
+#pragma unroll
+        for (int t = 0; t < CH; ++t) asm volatile("" : "+v"(xc[t]));
 #pragma unroll
         for (int t = 0; t < CH; ++t) {
             const int64_t c = lane + 64 * t;
-            if (c < nch) finish(c, cache[t], inv);
+            finish(c < nch ? c : nch - 1, xc[t], inv, c < nch);
+            if constexpr (kLdsAffine) asm volatile("" ::: "memory");
         }
     } else {
+        float inv = 1.0f;
         if (a.do_norm) {
-            for (int64_t c = lane; c < nch; c += 64)
-                ss += sumsq(c, load(c));
-#pragma unroll
-            for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
+            float ss = 0.0f;
+            for (int64_t c = lane; c < nch; c += 64) ss += sumsq(load_chunk(a, rb, c), c);
+            inv = rsqrt_mean(ss);
         }
-        const float inv = a.do_norm ? 1.0f / sqrtf(ss / (float)a.N + a.eps) : 1.0f;
-        for (int64_t c = lane; c < nch; c += 64)
-            finish(c, load(c), inv);
+        for (int64_t c = lane; c < nch; c += 64) finish(c, load_chunk(a, rb, c), inv, true);
     }
+}
+
+template <int DT, int CH>
+void launch_norm(const PostArgs& a, dim3 g, dim3 b, hipStream_t s) {
+    const size_t lds = post_lds_bytes(a);
+    if (a.bias || (a.do_norm && a.gamma)) hipLaunchKernelGGL((post_norm_kernel<DT, CH, true>), g, b, lds, s, a);
+    else hipLaunchKernelGGL((post_norm_kernel<DT, CH, false>), g, b, lds, s, a);
 }
 
 template <int DT>
 hipError_t launch_dt(const PostArgs& a, hipStream_t s) {
     const int64_t nch = a.N >> 3;
     const dim3 g((unsigned)((a.M + kRowsPerBlock - 1) / kRowsPerBlock)), b(kThreads);
-    if (nch <= 64 * 4) hipLaunchKernelGGL((post_kernel<DT, 4>), g, b, 0, s, a);
-    else if (nch <= 64 * 8) hipLaunchKernelGGL((post_kernel<DT, 8>), g, b, 0, s, a);
-    else if (nch <= 64 * 16) hipLaunchKernelGGL((post_kernel<DT, 16>), g, b, 0, s, a);
-    else hipLaunchKernelGGL((post_kernel<DT, 0>), g, b, 0, s, a);
+    if (!a.do_norm && !a.bias) hipLaunchKernelGGL((post_gather_kernel<DT>), g, b, post_lds_bytes(a), s, a);
+    else if (nch <= 64 * 4) launch_norm<DT, 4>(a, g, b, s);
+    else if (nch <= 64 * 8) launch_norm<DT, 8>(a, g, b, s);
+    else if (nch <= kMaxRegChunks) launch_norm<DT, 16>(a, g, b, s);
+    else launch_norm<DT, 0>(a, g, b, s);
     return hipGetLastError();
 }
 
 }  // namespace
+
+size_t post_lds_bytes(const PostArgs& a) {
+    const int64_t nch = a.N >> 3;
+    const bool norm_path = a.do_norm || a.bias;
+    const bool lds_affine = norm_path && (a.bias || (a.do_norm && a.gamma)) && nch <= kMaxRegChunks;
+    return (size_t)kRowsPerBlock * a.tiles_n * sizeof(uint32_t) + (lds_affine ? 2 * (size_t)nch * 16 : 0);
+}
 
 hipError_t launch_post(int dtype, const PostArgs& a, hipStream_t s) {
     if (a.M == 0 || a.N == 0) return hipSuccess;

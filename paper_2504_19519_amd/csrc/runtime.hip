@@ -312,6 +312,8 @@ fo_status fo_post_reorder(const fo_plan* plan, const void* dev_plan, const void*
         a.cpt_log2 = -1;
         for (int l = 0; l < 31; ++l)
             if ((1 << l) == cpt) a.cpt_log2 = l;
+        if (plan->pattern != FO_PATTERN_ROWMAJOR && (plan->tile_n % 8 || a.cpt_log2 < 0))
+            return fo::fail(FO_ERR_UNSUPPORTED, "post-reorder needs tile_n / 8 to be a power of two");
     }
     a.pattern = plan->pattern; a.num_dest = plan->num_dest;
     a.per_dest = plan->pattern == FO_PATTERN_SUBTILE
@@ -326,6 +328,11 @@ fo_status fo_post_reorder(const fo_plan* plan, const void* dev_plan, const void*
     }
     a.eps = eps;
     a.do_norm = do_rmsnorm ? 1 : 0;
+    // source pieces are addressed in 16-byte chunks with 32-bit offsets
+    if (std::max<int64_t>(plan->dest_elems, plan->M * plan->N) / 8 > (int64_t)UINT32_MAX)
+        return fo::fail(FO_ERR_SHAPE, "post-reorder source buffer too large for 32-bit chunk offsets");
+    if (fo::post_lds_bytes(a) > 64 * 1024)
+        return fo::fail(FO_ERR_UNSUPPORTED, "post-reorder: too many tile columns or too wide a row for LDS");
     hipError_t e = fo::launch_post(plan->dtype, a, (hipStream_t)stream);
     return e == hipSuccess ? FO_OK : fo::hip_fail("post-reorder launch", e);
 }
