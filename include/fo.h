@@ -146,6 +146,37 @@ typedef struct fo_plan fo_plan;   /* opaque, library-owned host memory */
 fo_status fo_plan_groups(const fo_problem* problem, const fo_grouping* grouping, fo_plan** out);
 void fo_plan_destroy(fo_plan* plan);
 
+/*
+ * Plan cache for shapes that vary at run time (Section 4.2, online stage: for
+ * dynamic tasks the search is run ahead of time for representative GEMM
+ * sizes, and an unseen size takes the partition of its nearest neighbour).
+ *
+ * A family is every fo_problem field but M and row_bucket (dest_perm compared
+ * by content). fo_plan_cache_add builds the plan of `problem` with `grouping`
+ * (the Algorithm 1 search when num_groups == 0, else the given partition,
+ * which must be in waves) and keeps its wave partition, replacing an entry of
+ * the same family and M. fo_plan_cache_lookup picks, among the entries of the
+ * problem's family, the one whose M is nearest (the smaller M on ties), maps
+ * its partition onto the problem's own wave count T (a cut after wave c moves
+ * to after wave round(c * T / T_ref), halves rounding up; cuts that land on 0,
+ * on T or on an earlier cut are dropped) and returns the plan built with it
+ * (free with fo_plan_destroy); *matched_m (may be NULL) receives the entry's M.
+ * The cache is host memory owned by the library; lookups do not modify it.
+ * Errors: FO_ERR_ARG (null argument, no entry of the family, a partition in
+ * tiles), and every error fo_plan_groups reports.
+ */
+typedef struct fo_plan_cache fo_plan_cache;
+fo_status fo_plan_cache_create(fo_plan_cache** out);
+void fo_plan_cache_destroy(fo_plan_cache* cache);
+fo_status fo_plan_cache_add(fo_plan_cache* cache, const fo_problem* problem, const fo_grouping* grouping);
+fo_status fo_plan_cache_lookup(const fo_plan_cache* cache, const fo_problem* problem, fo_plan** out,
+                               int64_t* matched_m);
+int32_t fo_plan_cache_size(const fo_plan_cache* cache);
+/* Entry e (0 <= e < size): its M and wave partition (valid until the cache
+ * changes). */
+fo_status fo_plan_cache_entry(const fo_plan_cache* cache, int32_t e, int64_t* M, int32_t* num_groups,
+                              const int32_t** sizes);
+
 /* Plan accessors. Arrays stay valid until fo_plan_destroy. */
 int32_t fo_plan_num_tiles(const fo_plan* plan);
 int32_t fo_plan_wave_width(const fo_plan* plan);      /* W                        */

@@ -20,7 +20,8 @@ What it computes, each part citing the passage it follows:
   tile (AllReduce), subtile (ReduceScatter) and subtoken (All-to-All)
   patterns, the contiguous (offset, length) segment each group hands to the
   communication, and the post-communication gather back to row-major order.
-* Predictive search over wave-group partitions (Section 4.1, Algorithm 1).
+* Predictive search over wave-group partitions (Section 4.1, Algorithm 1), and
+  the reuse of searched partitions by nearest size (Section 4.2).
 
 Readings of points the paper leaves open are listed in the module-level
 constants' comments and in the function docstrings; they match the readings
@@ -465,6 +466,48 @@ def search_partition(plan: Plan, gemm_us: float, curve_bytes, curve_us,
         return lambda j: lat[j]
 
     return predictive_search(T, gemm_us, comm_for, s_first, s_last)
+
+
+# --------------------------------------------------------------------------
+# Partitions reused across sizes (Section 4.2, online stage)
+# --------------------------------------------------------------------------
+
+def nearest_size(cached_ms: Sequence[int], M: int) -> int:
+    """Section 4.2: for dynamic shapes the search runs ahead of time on
+    representative GEMM sizes and an unseen size takes the partition of its
+    nearest neighbour. Reading: neighbours are sizes of the same problem
+    family (every parameter but M equal), the distance is |M - M_ref|, and a
+    tie goes to the smaller M_ref."""
+    best = None
+    for m in cached_ms:
+        if best is None or abs(M - m) < abs(M - best) or (abs(M - m) == abs(M - best) and m < best):
+            best = m
+    if best is None:
+        raise KeyError("no cached size")
+    return best
+
+
+def rescale_partition(sizes_ref: Sequence[int], T: int) -> Tuple[int, ...]:
+    """The nearest neighbour's partition applied to a problem of T waves.
+    Reading (the paper reuses the partition without saying how a different
+    wave count is handled): group boundaries keep their relative position. A
+    boundary after wave b of the T_ref cached waves moves to after wave
+    b * T / T_ref, rounded to the nearest integer with halves rounded up;
+    boundaries that land on wave 0, on wave T or not after the previous kept
+    boundary are dropped."""
+    from fractions import Fraction
+    T_ref = sum(sizes_ref)
+    if T <= 0:
+        return ()
+    kept = []
+    b = 0
+    for s in list(sizes_ref)[:-1]:
+        b += s
+        nb = math.floor(Fraction(b * T, T_ref) + Fraction(1, 2))
+        if 0 < nb < T and (not kept or nb > kept[-1]):
+            kept.append(nb)
+    edges = [0] + kept + [T]
+    return tuple(edges[i + 1] - edges[i] for i in range(len(edges) - 1))
 
 
 # --------------------------------------------------------------------------

@@ -18,7 +18,7 @@ from typing import Optional, Sequence
 import numpy as np
 
 __all__ = [
-    "FoError", "Plan", "plan_groups", "gemm_signal_reorder", "consume_group",
+    "FoError", "Plan", "PlanCache", "plan_groups", "gemm_signal_reorder", "consume_group",
     "post_reorder", "reset_counters", "run_overlapped", "set_poll_timeout_us",
     "get_poll_timeout_us", "device_num_cus", "set_sync_mode", "get_sync_mode",
     "set_consumer_grid", "get_consumer_grid", "set_tile_trace", "device_wall_clock_khz", "LIB_PATH",
@@ -82,6 +82,12 @@ def lib() -> ctypes.CDLL:
     pi64 = ctypes.POINTER(ctypes.c_int64)
     L.fo_plan_groups.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Grouping), ctypes.POINTER(vp)]
     L.fo_plan_destroy.argtypes = [vp]
+    L.fo_plan_cache_create.argtypes = [ctypes.POINTER(vp)]
+    L.fo_plan_cache_destroy.argtypes = [vp]
+    L.fo_plan_cache_add.argtypes = [vp, ctypes.POINTER(_Problem), ctypes.POINTER(_Grouping)]
+    L.fo_plan_cache_lookup.argtypes = [vp, ctypes.POINTER(_Problem), ctypes.POINTER(vp), pi64]
+    L.fo_plan_cache_size.argtypes, L.fo_plan_cache_size.restype = [vp], i32
+    L.fo_plan_cache_entry.argtypes = [vp, i32, pi64, pi32, ctypes.POINTER(pi32)]
     for name in ("num_tiles", "wave_width", "num_waves", "num_groups", "num_counters", "num_segments"):
         f = getattr(L, f"fo_plan_{name}")
         f.argtypes, f.restype = [vp], i32
@@ -111,6 +117,8 @@ def lib() -> ctypes.CDLL:
     L.fo_device_num_cus.argtypes = [i32, pi32]
     L.fo_status_string.argtypes, L.fo_status_string.restype = [ctypes.c_int], ctypes.c_char_p
     L.fo_last_error.restype = ctypes.c_char_p
+    for f in (L.fo_plan_cache_create, L.fo_plan_cache_add, L.fo_plan_cache_lookup, L.fo_plan_cache_entry):
+        f.restype = ctypes.c_int
     for f in (L.fo_plan_groups, L.fo_plan_to_device, L.fo_gemm_signal_reorder, L.fo_consume_group,
               L.fo_post_reorder, L.fo_reset_counters, L.fo_run_overlapped, L.fo_device_num_cus):
         f.restype = ctypes.c_int
@@ -250,15 +258,11 @@ class Plan:
         _check(lib().fo_plan_to_device(self._h, _ptr(dev_buf), nb, _stream(stream)))
 
 
-def plan_groups(M: int, N: int, K: int, *, dtype="fp16", tile_m: int = 256, tile_n: int = 128,
-                order="xcd", group_m: int = 4, num_xcds: int = 8, num_cus: int = 256,
-                wg_per_cu: int = 1, reserved_cus: int = 0, pattern="tile", num_dest: int = 0,
-                dest_perm: Optional[Sequence[int]] = None, row_bucket=None,
-                sizes: Optional[Sequence[int]] = None, unit="waves", gemm_us: float = 0.0,
-                curve_bytes=None, curve_us=None, s_first: int = 2, s_last: int = 4) -> Plan:
-    """fo_plan_groups: sizes=None runs the Algorithm 1 search (needs gemm_us
-    and the latency curve)."""
-    L = lib()
+def _problem(M: int, N: int, K: int, *, dtype="fp16", tile_m: int = 256, tile_n: int = 128,
+             order="xcd", group_m: int = 4, num_xcds: int = 8, num_cus: int = 256,
+             wg_per_cu: int = 1, reserved_cus: int = 0, pattern="tile", num_dest: int = 0,
+             dest_perm: Optional[Sequence[int]] = None, row_bucket=None):
+    """An fo_problem and the arrays it points to (keep them alive with it)."""
     perm = _i32_array(dest_perm)
     buck = _i32_array(row_bucket)
     prob = _Problem(M=M, N=N, K=K, dtype=_DTYPES[dtype], tile_m=tile_m, tile_n=tile_n,
@@ -267,6 +271,12 @@ def plan_groups(M: int, N: int, K: int, *, dtype="fp16", tile_m: int = 256, tile
                     num_dest=num_dest,
                     dest_perm=ctypes.cast(perm, ctypes.POINTER(ctypes.c_int32)) if perm is not None else None,
                     row_bucket=ctypes.cast(buck, ctypes.POINTER(ctypes.c_int32)) if buck is not None else None)
+    return prob, (perm, buck)
+
+
+def _grouping(sizes: Optional[Sequence[int]] = None, unit="waves", gemm_us: float = 0.0,
+              curve_bytes=None, curve_us=None, s_first: int = 2, s_last: int = 4):
+    """An fo_grouping and the arrays it points to."""
     sz = _i32_array(sizes)
     cb, cu = _f64_array(curve_bytes), _f64_array(curve_us)
     grp = _Grouping(unit=_UNITS[unit], num_groups=0 if sizes is None else len(sizes),
@@ -276,9 +286,81 @@ def plan_groups(M: int, N: int, K: int, *, dtype="fp16", tile_m: int = 256, tile
                     curve_us=ctypes.cast(cu, ctypes.POINTER(ctypes.c_double)) if cu is not None else None,
                     curve_len=0 if curve_bytes is None else len(curve_bytes),
                     s_first=s_first, s_last=s_last)
+    return grp, (sz, cb, cu)
+
+
+_PROBLEM_KEYS = ("dtype", "tile_m", "tile_n", "order", "group_m", "num_xcds", "num_cus", "wg_per_cu",
+                 "reserved_cus", "pattern", "num_dest", "dest_perm", "row_bucket")
+
+
+def _split(kw):
+    prob_kw = {k: v for k, v in kw.items() if k in _PROBLEM_KEYS}
+    grp_kw = {k: v for k, v in kw.items() if k not in _PROBLEM_KEYS}
+    return prob_kw, grp_kw
+
+
+def _plan_of(handle: int, M: int, N: int, K: int, prob_kw) -> Plan:
+    return Plan(handle, M, N, K, _DTYPES[prob_kw.get("dtype", "fp16")], prob_kw.get("tile_m", 256),
+                prob_kw.get("tile_n", 128), _PATTERNS[prob_kw.get("pattern", "tile")], prob_kw.get("num_dest", 0))
+
+
+def plan_groups(M: int, N: int, K: int, **kw) -> Plan:
+    """fo_plan_groups. Keywords: the fo_problem fields (dtype, tile_m, tile_n,
+    order, group_m, num_xcds, num_cus, wg_per_cu, reserved_cus, pattern,
+    num_dest, dest_perm, row_bucket) and the fo_grouping ones (sizes, unit,
+    gemm_us, curve_bytes, curve_us, s_first, s_last); sizes=None runs the
+    Algorithm 1 search (needs gemm_us and the latency curve)."""
+    L = lib()
+    prob_kw, grp_kw = _split(kw)
+    prob, keep_p = _problem(M, N, K, **prob_kw)
+    grp, keep_g = _grouping(**grp_kw)
     out = ctypes.c_void_p()
     _check(L.fo_plan_groups(ctypes.byref(prob), ctypes.byref(grp), ctypes.byref(out)))
-    return Plan(out.value, M, N, K, _DTYPES[dtype], tile_m, tile_n, _PATTERNS[pattern], num_dest)
+    return _plan_of(out.value, M, N, K, prob_kw)
+
+
+class PlanCache:
+    """fo_plan_cache: partitions searched ahead of time for representative
+    sizes of a problem family, reused by nearest M for unseen sizes (Section
+    4.2, online stage)."""
+
+    def __init__(self):
+        L = lib()
+        h = ctypes.c_void_p()
+        _check(L.fo_plan_cache_create(ctypes.byref(h)))
+        self._h = h
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.fo_plan_cache_destroy(h)
+            self._h = None
+
+    def add(self, M: int, N: int, K: int, **kw) -> None:
+        """fo_plan_cache_add: same keywords as plan_groups."""
+        prob_kw, grp_kw = _split(kw)
+        prob, keep_p = _problem(M, N, K, **prob_kw)
+        grp, keep_g = _grouping(**grp_kw)
+        _check(lib().fo_plan_cache_add(self._h, ctypes.byref(prob), ctypes.byref(grp)))
+
+    def lookup(self, M: int, N: int, K: int, **kw):
+        """fo_plan_cache_lookup: (Plan, M of the entry used)."""
+        prob, keep_p = _problem(M, N, K, **kw)
+        out, matched = ctypes.c_void_p(), ctypes.c_int64()
+        _check(lib().fo_plan_cache_lookup(self._h, ctypes.byref(prob), ctypes.byref(out), ctypes.byref(matched)))
+        return _plan_of(out.value, M, N, K, kw), int(matched.value)
+
+    def __len__(self) -> int:
+        return int(lib().fo_plan_cache_size(self._h))
+
+    def entries(self):
+        """[(M, wave partition)] in insertion order."""
+        L, res = lib(), []
+        for e in range(len(self)):
+            m, n, sz = ctypes.c_int64(), ctypes.c_int32(), ctypes.POINTER(ctypes.c_int32)()
+            _check(L.fo_plan_cache_entry(self._h, e, ctypes.byref(m), ctypes.byref(n), ctypes.byref(sz)))
+            res.append((int(m.value), [int(sz[j]) for j in range(n.value)]))
+        return res
 
 
 def gemm_signal_reorder(plan: Plan, dev_plan, A, W, C_out, counters=None, stream=None) -> None:

@@ -10,6 +10,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <limits>
 #include <new>
 
@@ -315,7 +316,62 @@ fo_status build(fo_plan& p, const fo_problem& pr, const fo_grouping& g) {
     return FO_OK;
 }
 
+// Partition of T_new waves that keeps the relative cut positions of `ref`
+// (a partition of T_ref waves): a cut after wave c becomes a cut after wave
+// round(c * T_new / T_ref) (halves round up); cuts that fall on 0 or T_new,
+// or on an earlier cut, are dropped.
+std::vector<int32_t> map_partition(const std::vector<int32_t>& ref, int32_t t_new) {
+    int64_t t_ref = 0;
+    for (int32_t s : ref) t_ref += s;
+    std::vector<int32_t> out;
+    if (t_new <= 0) return out;
+    if (t_ref <= 0) return {t_new};
+    int64_t cut = 0;
+    int32_t prev = 0;
+    for (size_t j = 0; j + 1 < ref.size(); ++j) {
+        cut += ref[j];
+        const int32_t c = (int32_t)((2 * cut * t_new + t_ref) / (2 * t_ref));
+        if (c <= prev || c >= t_new) continue;
+        out.push_back(c - prev);
+        prev = c;
+    }
+    out.push_back(t_new - prev);
+    return out;
+}
+
+// Everything of a problem but M (and the per-row bucket map, which has M
+// entries): problems of one family share cached partitions.
+bool same_family(const fo_problem& a, const fo_problem& b) {
+    if (a.N != b.N || a.K != b.K || a.dtype != b.dtype || a.tile_m != b.tile_m || a.tile_n != b.tile_n ||
+        a.order != b.order || a.num_cus != b.num_cus || a.wg_per_cu != b.wg_per_cu ||
+        a.reserved_cus != b.reserved_cus || a.pattern != b.pattern)
+        return false;
+    if (a.order != FO_ORDER_ROWMAJOR && a.group_m != b.group_m) return false;
+    if (a.order == FO_ORDER_XCD && a.num_xcds != b.num_xcds) return false;
+    const bool dest = a.pattern == FO_PATTERN_SUBTILE || a.pattern == FO_PATTERN_SUBTOKEN;
+    if (dest && a.num_dest != b.num_dest) return false;
+    if (a.pattern == FO_PATTERN_SUBTILE) {
+        for (int k = 0; k < a.num_dest; ++k) {
+            const int32_t x = a.dest_perm ? a.dest_perm[k] : k, y = b.dest_perm ? b.dest_perm[k] : k;
+            if (x != y) return false;
+        }
+    }
+    return true;
+}
+
 }  // namespace
+
+// One cached partition: the problem it was searched for (dest_perm copied,
+// no bucket map) and its wave groups.
+struct fo_cached_partition {
+    fo_problem problem;
+    std::vector<int32_t> dest_perm;
+    std::vector<int32_t> sizes;
+};
+
+struct fo_plan_cache {
+    std::vector<fo_cached_partition> entries;
+};
 
 extern "C" {
 
@@ -339,6 +395,95 @@ fo_status fo_plan_groups(const fo_problem* problem, const fo_grouping* grouping,
 }
 
 void fo_plan_destroy(fo_plan* plan) { delete plan; }
+
+fo_status fo_plan_cache_create(fo_plan_cache** out) {
+    fo::clear_error();
+    if (!out) return fo::fail(FO_ERR_ARG, "null argument");
+    *out = new (std::nothrow) fo_plan_cache();
+    return *out ? FO_OK : fo::fail(FO_ERR_ARG, "out of host memory");
+}
+
+void fo_plan_cache_destroy(fo_plan_cache* cache) { delete cache; }
+
+fo_status fo_plan_cache_add(fo_plan_cache* cache, const fo_problem* problem, const fo_grouping* grouping) {
+    fo::clear_error();
+    if (!cache || !problem || !grouping) return fo::fail(FO_ERR_ARG, "null argument");
+    if (grouping->num_groups > 0 && grouping->unit != FO_UNIT_WAVES)
+        return fo::fail(FO_ERR_ARG, "cached partitions are given in waves");
+    fo_plan* p = nullptr;
+    fo_status st = fo_plan_groups(problem, grouping, &p);
+    if (st != FO_OK) return st;
+    try {
+        fo_cached_partition e;
+        e.problem = *problem;
+        e.problem.row_bucket = nullptr;
+        e.dest_perm = p->dest_perm;
+        e.problem.dest_perm = nullptr;
+        e.sizes = p->sizes;
+        delete p;
+        for (auto& old : cache->entries) {
+            fo_problem q = old.problem;
+            q.dest_perm = old.dest_perm.empty() ? nullptr : old.dest_perm.data();
+            fo_problem r = e.problem;
+            r.dest_perm = e.dest_perm.empty() ? nullptr : e.dest_perm.data();
+            if (q.M == r.M && same_family(q, r)) {      // replace the entry of the same size
+                old = std::move(e);
+                return FO_OK;
+            }
+        }
+        cache->entries.push_back(std::move(e));
+    } catch (const std::bad_alloc&) {
+        return fo::fail(FO_ERR_ARG, "out of host memory");
+    }
+    return FO_OK;
+}
+
+fo_status fo_plan_cache_lookup(const fo_plan_cache* cache, const fo_problem* problem, fo_plan** out,
+                               int64_t* matched_m) {
+    fo::clear_error();
+    if (!cache || !problem || !out) return fo::fail(FO_ERR_ARG, "null argument");
+    const fo_cached_partition* best = nullptr;
+    for (const auto& e : cache->entries) {
+        fo_problem q = e.problem;
+        q.dest_perm = e.dest_perm.empty() ? nullptr : e.dest_perm.data();
+        if (!same_family(q, *problem)) continue;
+        const int64_t d = std::llabs(q.M - problem->M), db = best ? std::llabs(best->problem.M - problem->M) : 0;
+        if (!best || d < db || (d == db && q.M < best->problem.M)) best = &e;
+    }
+    if (!best) return fo::fail(FO_ERR_ARG, "no cached partition for this problem family");
+    if (problem->tile_m < 1 || problem->tile_n < 1 || problem->num_cus <= problem->reserved_cus ||
+        problem->wg_per_cu < 1 || problem->M < 0 || problem->N < 0)
+        return fo::fail(FO_ERR_ARG, "bad problem");
+    const int64_t tiles = (problem->M / problem->tile_m) * (problem->N / problem->tile_n);
+    const int64_t W = (int64_t)(problem->num_cus - problem->reserved_cus) * problem->wg_per_cu;
+    const int32_t T = (int32_t)((tiles + W - 1) / W);
+    std::vector<int32_t> sizes;
+    try {
+        sizes = map_partition(best->sizes, T);
+    } catch (const std::bad_alloc&) {
+        return fo::fail(FO_ERR_ARG, "out of host memory");
+    }
+    fo_grouping g{};
+    g.unit = FO_UNIT_WAVES;
+    g.num_groups = (int32_t)sizes.size();
+    g.sizes = sizes.empty() ? nullptr : sizes.data();     // no tiles: no groups
+    const fo_status st = fo_plan_groups(problem, &g, out);
+    if (st == FO_OK && matched_m) *matched_m = best->problem.M;
+    return st;
+}
+
+int32_t fo_plan_cache_size(const fo_plan_cache* cache) { return cache ? (int32_t)cache->entries.size() : 0; }
+
+fo_status fo_plan_cache_entry(const fo_plan_cache* cache, int32_t e, int64_t* M, int32_t* num_groups,
+                              const int32_t** sizes) {
+    fo::clear_error();
+    if (!cache || e < 0 || e >= (int32_t)cache->entries.size()) return fo::fail(FO_ERR_ARG, "no such entry");
+    const auto& x = cache->entries[e];
+    if (M) *M = x.problem.M;
+    if (num_groups) *num_groups = (int32_t)x.sizes.size();
+    if (sizes) *sizes = x.sizes.data();
+    return FO_OK;
+}
 
 int32_t fo_plan_num_tiles(const fo_plan* p) { return p ? p->tiles : 0; }
 int32_t fo_plan_wave_width(const fo_plan* p) { return p ? p->W : 0; }

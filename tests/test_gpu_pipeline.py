@@ -229,3 +229,31 @@ def test_consumer_grid(grid, name):
         check(w, inp, plan, o)
     finally:
         fo.set_consumer_grid(*old)
+
+
+@pytest.mark.parametrize("name", ["rs_8192x8192x3584", "a2a_4096x7168x2048"])
+def test_plan_from_cache_runs_the_path(name):
+    # a size seen only at run time takes the partition cached for its nearest
+    # neighbour (Section 4.2); the plan built from it runs the whole path
+    M, N, K, cus, _ = SMALL[name]
+    w = workloads.WORKLOADS[name].with_shape(M, N, K)
+    say(f"[pipeline plan cache] {w.name}")
+    inp = workloads.make_inputs(w)
+    nd = w.num_dest
+    kw = dict(dtype=w.dtype, tile_m=w.tile_m, tile_n=w.tile_n, order=w.order, num_cus=cus,
+              pattern=w.pattern, num_dest=nd, dest_perm=inp.sigma if w.pattern == "subtile" else None)
+    rng = np.random.default_rng(7)
+    cache = fo.PlanCache()
+    waves = lambda m: -(-(m // w.tile_m) * (N // w.tile_n) // cus)
+    cached = {512: oracle.rescale_partition((1, 1), waves(512)),
+              2048: oracle.rescale_partition((1, 2, 2), waves(2048))}
+    for m, sizes in cached.items():
+        bucket = rng.integers(0, nd, m) if w.pattern == "subtoken" else None
+        cache.add(m, N, K, sizes=list(sizes), row_bucket=bucket, **kw)
+    plan, matched = cache.lookup(M, N, K, row_bucket=inp.bucket if w.pattern == "subtoken" else None, **kw)
+    assert matched == oracle.nearest_size(list(cached), M)
+    sizes = oracle.rescale_partition(cached[matched], plan.T)
+    assert tuple(plan.sizes) == sizes
+    o = oracle.make_plan(w.M, w.N, w.tile_m, w.tile_n, num_cus=cus, order=w.order, pattern=w.pattern,
+                         num_dest=nd, sigma=inp.sigma, bucket=inp.bucket, sizes=sizes, unit="waves")
+    check(w, inp, plan, o)
