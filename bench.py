@@ -182,6 +182,57 @@ def timed_steps(torch, w, plan, dp, b, s1, s2, steps, warmup):
     return step_us, float(np.mean(gemm)), float(np.median(gemm)), wall
 
 
+def planner_report(w, inp, num_cus, gemm_us, curve):
+    """Host cost of the planner's online stage (Section 4.2): Algorithm 1 on
+    this workload vs. a lookup in a plan cache filled ahead of time for
+    representative sizes of the same family (M/4, M/2, 2M; the GEMM time
+    scaled with M), and the estimated latency of the cached partitions at
+    unseen sizes against the search's own optimum there."""
+    xs, ys = curve
+    kw = dict(dtype=w.dtype, tile_m=w.tile_m, tile_n=w.tile_n, order=w.order, num_cus=num_cus,
+              pattern=w.pattern, num_dest=w.num_dest if w.pattern in ("subtile", "subtoken") else 0,
+              dest_perm=inp.sigma if w.pattern == "subtile" else None)
+    rng = np.random.default_rng(w.seed + 11)
+
+    def bucket(M):
+        return rng.integers(0, w.num_dest, M) if w.pattern == "subtoken" else None
+
+    def search(M, b):
+        return fo.plan_groups(M, w.N, w.K, row_bucket=b, sizes=None, gemm_us=gemm_us * M / w.M,
+                              curve_bytes=xs, curve_us=ys, s_first=2, s_last=4, **kw)
+
+    b = bucket(w.M)
+    reps = 20
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        search(w.M, b)
+    search_us = (time.perf_counter() - t0) / reps * 1e6
+    cache = fo.PlanCache()
+    reps_m = [m for m in (w.M // 4, w.M // 2, 2 * w.M) if m % w.tile_m == 0 and m > 0]
+    for m in reps_m:
+        cache.add(m, w.N, w.K, row_bucket=bucket(m), sizes=None, gemm_us=gemm_us * m / w.M,
+                  curve_bytes=xs, curve_us=ys, s_first=2, s_last=4, **kw)
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        cache.lookup(w.M, w.N, w.K, row_bucket=b, **kw)
+    lookup_us = (time.perf_counter() - t0) / reps * 1e6
+    unseen = []
+    for frac in (3, 5, 6, 7):          # M * frac / 4: between and beyond the cached sizes
+        m = w.M * frac // 4
+        if m % w.tile_m:
+            continue
+        bm = bucket(m)
+        plan, matched = cache.lookup(m, w.N, w.K, row_bucket=bm, **kw)
+        est = fo.plan_groups(m, w.N, w.K, row_bucket=bm, sizes=list(plan.sizes), gemm_us=gemm_us * m / w.M,
+                             curve_bytes=xs, curve_us=ys, **kw).predicted_us
+        best = search(m, bm)
+        unseen.append({"M": m, "matched_M": matched, "cached_groups": [int(x) for x in plan.sizes],
+                       "searched_groups": [int(x) for x in best.sizes],
+                       "estimate_cached_over_searched": round(est / best.predicted_us, 4)})
+    return {"search_us": round(search_us, 1), "cache_lookup_us": round(lookup_us, 1),
+            "cached_sizes_M": reps_m, "unseen": unseen}
+
+
 def traffic_bytes(w):
     """HBM bytes per GEMM launch (FETCH_SIZE + WRITE_SIZE, scaled by a plain
     copy of known size) from the committed rocprofv3 summary of this
@@ -447,6 +498,7 @@ def main():
     dp = dev_plan(torch, plan)
     torch.cuda.synchronize()
     log(f"plan: T={plan.T} groups={list(plan.sizes)} predicted {plan.predicted_us:.1f} us")
+    planner = planner_report(w, inp, num_cus, sig_us, (xs, ys)) if not args.sizes else None
 
     # ---- timed steps -----------------------------------------------------
     # overlapped vs serialized, in alternating rounds so that both see the
@@ -599,6 +651,7 @@ def main():
                                      "collectives; not comparable to this 1-GPU stand-in)"},
         "sweep_waves_per_group": sweep,
         "predictor": None if pred is None else {k: v for k, v in pred.items() if k != "phase"},
+        "planner": planner,
         "sync_modes": {"default": list(default_modes), "variants": sync_variants,
                        "overlapped_equals_serial_bits": consistent},
         "consumer_grid": {"default": "%dx%d" % default_grid, "variants": grid_variants},
