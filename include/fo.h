@@ -301,8 +301,11 @@ fo_status fo_consume_group(const void* src, const void* peer, void* dst, int64_t
  * Then, row-wise: h = x + bias (bias [N] or NULL), and if do_rmsnorm:
  * y = h / sqrt(mean_n(h^2) + eps) * gamma (gamma [N] or NULL = 1), in fp32,
  * rounded once to the dtype; else y = h.
- * Errors: FO_ERR_ARG, FO_ERR_UNSUPPORTED (N % 8 or tile_n % 8 not zero),
- * FO_ERR_HIP.
+ * Errors: FO_ERR_ARG, FO_ERR_UNSUPPORTED (N % 8 or tile_n % 8 not zero;
+ * a reordered pattern whose tile_n / 8 is not a power of two; more than 64 KB
+ * of LDS per workgroup: 16 * tiles_n bytes of source offsets, plus 4 * N bytes
+ * of bias and gamma when rows of up to 8192 columns are normalised),
+ * FO_ERR_SHAPE (a source buffer of 2^32 or more 16-byte chunks), FO_ERR_HIP.
  */
 fo_status fo_post_reorder(const fo_plan* plan, const void* dev_plan, const void* src,
                           void* out, const void* bias, const void* gamma, float eps,
