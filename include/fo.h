@@ -183,9 +183,13 @@ int32_t fo_plan_wave_width(const fo_plan* plan);      /* W                      
 int32_t fo_plan_num_waves(const fo_plan* plan);       /* T                        */
 int32_t fo_plan_num_groups(const fo_plan* plan);      /* P                        */
 /* Length of the counters array of a signalling run: P group counters, then
- * FO_DISPENSER_WORDS tile-position counters of the GEMM. */
+ * FO_DISPENSER_WORDS tile-position counters of the GEMM, then
+ * FO_HANDOFF_WORDS words that fo_run_overlapped uses to hand work between
+ * its two streams. */
 #define FO_DISPENSER_WORDS 8
-int32_t fo_plan_num_counters(const fo_plan* plan);    /* P + FO_DISPENSER_WORDS   */
+#define FO_HANDOFF_WORDS 2
+int32_t fo_plan_num_counters(const fo_plan* plan);    /* P + FO_DISPENSER_WORDS
+                                                         + FO_HANDOFF_WORDS       */
 const int32_t* fo_plan_group_sizes(const fo_plan* plan);   /* [P], in the plan's unit */
 const int32_t* fo_plan_order(const fo_plan* plan);         /* [tiles] position -> tile */
 const int32_t* fo_plan_tile_to_slot(const fo_plan* plan);  /* [tiles] the reorder map  */
@@ -247,9 +251,10 @@ fo_status fo_plan_to_device(const fo_plan* plan, void* dev_buf, size_t bytes, vo
  *             (tm, tn) in slot s goes to subtoken pool_off[b] +
  *             pool_base[s*B+b] + (rank of row r among rows of tile row tm
  *             bound for b), b = row_bucket[tm*tile_m + r].
- * counters: fo_plan_num_counters(plan) = P + FO_DISPENSER_WORDS uint32,
- * zeroed by the caller before the launch and before any consumer of this run
- * starts (see fo_reset_counters); NULL = no signalling. When a tile's stores
+ * counters: at least P + FO_DISPENSER_WORDS uint32 (fo_plan_num_counters
+ * also counts the words fo_run_overlapped needs), zeroed by the caller before
+ * the launch and before any consumer of this run starts (see
+ * fo_reset_counters); NULL = no signalling. When a tile's stores
  * are complete, one workgroup-level agent-scope release increment is made on
  * counters[group of its slot]; when the GEMM is done, counters[j] ==
  * target_j for every j < P. counters[P ..] hand out tile positions to the
@@ -319,24 +324,42 @@ fo_status fo_reset_counters(uint32_t* counters, int32_t n, void* stream);
 /*
  * One overlapped run of the whole path (Section 5: GEMM on one stream, the
  * signalling + communication on another; Figure 5 order):
- *   gemm_stream: reset counters + status -> event E0 -> GEMM (signalling)
- *   comm_stream: wait E0 -> one consumer launch per group -> event E1
- *   gemm_stream: wait E1 -> fo_post_reorder (if out != NULL)
+ *   gemm_stream: reset kernel -> GEMM (signalling) -> done wait
+ *                -> fo_post_reorder (if out != NULL)
+ *   comm_stream: gate kernel -> one consumer launch per group
+ * The two streams hand work to each other on the device, not with events:
+ * the reset kernel zeroes the status word and counters[0, P +
+ * FO_DISPENSER_WORDS + 2) except the gate word counters[P +
+ * FO_DISPENSER_WORDS], then writes a tag unique to the run into the gate
+ * word, and the gate kernel (one wave) holds the consumers until it reads
+ * that tag; the final consumer launch adds its finished workgroups into
+ * counters[P + FO_DISPENSER_WORDS + 1], and the done wait (one wave) holds
+ * the post-reorder until all have. Both waits are bounded like a consumer's
+ * (fo_set_poll_timeout_us): on timeout bit 0 of the status word is set and
+ * the run's dst and out are unspecified.
  * A group's consumer is one wait kernel on the group's counter and one
  * streaming kernel that does what fo_consume_group does for each of the
  * group's plan segments (fo_plan_segments: 1, R or B of them). Every group
  * but the last uses the grid of fo_get_consumer_grid(); the last group,
  * which runs after the GEMM, uses up to 256 workgroups of 256 threads (as do
  * all groups of a serialized run).
- * With comm_stream == gemm_stream (or NULL) the same work runs serialized.
+ * With comm_stream == gemm_stream (or NULL) the same work runs serialized
+ * on gemm_stream, without the handoffs. An overlapped run needs a created
+ * gemm_stream (not the null stream, which would wait for the gate kernel on
+ * a blocking comm_stream) and counters.
  * Buffers: C_out (GEMM output, see fo_gemm_signal_reorder), peer (NULL for
  * All-to-All; else the peer's partial in C_out's layout), dst
  * (fo_plan_dest_elems), out ([M, N] or NULL), counters
- * [fo_plan_num_counters], status_word [1].
+ * [fo_plan_num_counters] (zero when first used: the gate word must not hold
+ * another run's tag from an earlier allocation), status_word [1] or NULL.
+ * Once gemm_stream has passed the run, every kernel of the run has made its
+ * last memory access (comm_stream may still be retiring the final consumer
+ * launch's workgroups).
  * gemm_begin_event / gemm_end_event: optional caller-owned hipEvent_t (as
  * void*) recorded on gemm_stream right before and after the GEMM launch, so
  * a caller can time the GEMM inside the overlapped run; NULL = none.
- * Uses two library-owned HIP events per calling thread and device.
+ * Errors: FO_ERR_ARG (no plan or dst; overlapped without counters or with a
+ * null gemm_stream), and those of the three calls the run makes.
  */
 fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan,
                             const void* A, const void* W, void* C_out,

@@ -25,6 +25,7 @@ struct ConsumeArgs {
     uint32_t target;
     uint32_t* status;            // bit 0 set on a timed-out wait (may be nullptr)
     uint64_t timeout_ticks;      // wall-clock ticks
+    uint32_t* done;              // non-null: each workgroup adds 1 when its stores are visible
     int32_t nseg;                // 1 .. kMaxConsumeSegments
     ConsumeSegment seg[kMaxConsumeSegments];
 };
@@ -34,7 +35,22 @@ struct ConsumeArgs {
 // 64, 128 or 256. full: the launch has the device to itself (more accesses
 // in flight per thread); otherwise it runs beside the GEMM and keeps its
 // registers within what a SIMD running two GEMM waves has left.
+// *blocks (if non-null) receives the streaming kernel's grid size.
 hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blocks, int threads, bool full,
-                          hipStream_t s);
+                          hipStream_t s, int* blocks = nullptr);
+
+// One wave that polls until *counter >= target (bounded by timeout_ticks;
+// on timeout bit 0 of *status is raised).
+hipError_t launch_wait(const uint32_t* counter, uint32_t target, uint32_t* status, uint64_t timeout_ticks,
+                       hipStream_t s);
+
+// Tags of the start handoff of an overlapped run: the run's reset kernel
+// writes its tag into the gate word once the counters are zero; the gate
+// kernel on the other stream waits for that tag. A gate that times out
+// replaces the word's old value by tag | kGateTimedOut, which the reset
+// kernel, if it runs later, turns into bit 0 of the status word.
+constexpr uint32_t kGateTag = 0x80000000u;
+constexpr uint32_t kGateTimedOut = 0x40000000u;
+hipError_t launch_gate(uint32_t* gate, uint32_t tag, uint32_t* status, uint64_t timeout_ticks, hipStream_t s);
 
 }  // namespace fo

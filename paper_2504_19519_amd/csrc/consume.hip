@@ -40,6 +40,30 @@ constexpr int kRsrcWord3 = 0x00020000;
 // registers must leave room for the GEMM's waves on the same SIMD.
 constexpr int kUnrollFull = 4;
 constexpr int kUnrollBeside = 2;
+// s_waitcnt operand: vmcnt(0), other counters not waited for
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+// Destination stores. Nontemporal by default (the next kernel reads the data,
+// not this one). WT: device-coherent write-through stores (sc1), used by the
+// launch that counts its finished workgroups for a wait on another stream:
+// they reach the memory side that every chiplet shares, so once a wave's
+// stores are complete (vmcnt 0) they are visible device-wide and no L2
+// write-back is needed before the count.
+template <bool WT>
+__device__ __forceinline__ void put16(u32x4_t* p, u32x4_t v) {
+    if constexpr (WT) asm volatile("global_store_dwordx4 %0, %1, off sc1" : : "v"(p), "v"(v) : "memory");
+    else __builtin_nontemporal_store(v, p);
+}
+template <bool WT>
+__device__ __forceinline__ void put8(uint64_t* p, uint64_t v) {
+    if constexpr (WT) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else __builtin_nontemporal_store(v, p);
+}
+template <bool WT>
+__device__ __forceinline__ void put2(uint16_t* p, uint16_t v) {
+    if constexpr (WT) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else *p = v;
+}
 
 // The wait of a launch runs in a kernel of its own, one workgroup of one
 // wave, ahead of the streaming kernel on the same stream: one lane polls the
@@ -61,6 +85,33 @@ __global__ __launch_bounds__(64) void wait_kernel(const uint32_t* counter, uint3
             return;
         }
     }
+}
+
+// Start handoff of an overlapped run (one wave, on the consumer stream ahead
+// of the run's first consumer): lane 0 polls the gate word until it holds
+// the run's tag, which the run's reset kernel writes with a release once the
+// counters are zero and the previous run's post-reorder, ordered before it
+// on the GEMM stream, has finished reading the destination buffer. On
+// timeout the lane marks the word (compare-and-swap, so a tag that arrives
+// meanwhile still wins) and raises bit 0 of the status word.
+__global__ __launch_bounds__(64) void gate_kernel(uint32_t* gate, uint32_t tag, uint32_t* status,
+                                                  uint64_t timeout_ticks) {
+    if (threadIdx.x != 0) return;
+    uint32_t v = __hip_atomic_load(gate, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t t0 = wall_clock64();
+    while (v != tag) {
+        __builtin_amdgcn_s_sleep(8);
+        v = __hip_atomic_load(gate, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (v != tag && wall_clock64() - t0 > timeout_ticks) {
+            if (__hip_atomic_compare_exchange_strong(gate, &v, tag | kGateTimedOut, __ATOMIC_RELAXED,
+                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                if (status) __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                return;
+            }
+            // v now holds the word's current value; the loop re-checks it
+        }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 }
 
 // Start of a streaming workgroup: one read of the counter (the wait kernel
@@ -113,7 +164,7 @@ __device__ __forceinline__ uint16_t add1(uint16_t x, uint16_t y) {
 
 // Stream one segment, 16 bytes per lane per access (FENCE_ALL / FENCE_ONE;
 // src, peer and dst 16-byte aligned): nontemporal loads and stores.
-template <int DT, bool SUM, int kUnroll>
+template <int DT, bool SUM, int kUnroll, bool WT>
 __device__ __forceinline__ void stream_vec16(const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer,
                                              uint16_t* __restrict__ dst, int64_t len) {
     const int64_t n16 = len >> 3;
@@ -133,24 +184,24 @@ __device__ __forceinline__ void stream_vec16(const uint16_t* __restrict__ src, c
             for (int u = 0; u < kUnroll; ++u) x[u] = add8<DT>(x[u], y[u]);
         }
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) __builtin_nontemporal_store(x[u], d + i + u * stride);
+        for (int u = 0; u < kUnroll; ++u) put16<WT>(d + i + u * stride, x[u]);
     }
     for (; i < n16; i += stride) {
         u32x4_t x = __builtin_nontemporal_load(s + i);
         if constexpr (SUM) x = add8<DT>(x, __builtin_nontemporal_load(q + i));
-        __builtin_nontemporal_store(x, d + i);
+        put16<WT>(d + i, x);
     }
     // ragged tail (< 8 elements)
     if (blockIdx.x == 0 && threadIdx.x < (len & 7)) {
         const int64_t e = (n16 << 3) + threadIdx.x;
-        dst[e] = SUM ? add1<DT>(src[e], peer[e]) : src[e];
+        put2<WT>(dst + e, SUM ? add1<DT>(src[e], peer[e]) : src[e]);
     }
 }
 
 // Stream one segment with device-coherent 8-byte source loads (COHERENT;
 // src, peer and dst 8-byte aligned). Two 8-byte units per lane per
 // unrolled step.
-template <int DT, bool SUM, int kUnroll>
+template <int DT, bool SUM, int kUnroll, bool WT>
 __device__ __forceinline__ void stream_coherent8(const uint16_t* __restrict__ src,
                                                  const uint16_t* __restrict__ peer,
                                                  uint16_t* __restrict__ dst, int64_t len) {
@@ -180,18 +231,18 @@ __device__ __forceinline__ void stream_coherent8(const uint16_t* __restrict__ sr
             for (int u = 0; u < U; ++u) x[u] = add4(x[u], y[u]);
         }
 #pragma unroll
-        for (int u = 0; u < U; ++u) __builtin_nontemporal_store(x[u], d + i + u * stride);
+        for (int u = 0; u < U; ++u) put8<WT>(d + i + u * stride, x[u]);
     }
     for (; i < n8; i += stride) {
         uint64_t x = __hip_atomic_load(s + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if constexpr (SUM) x = add4(x, __builtin_nontemporal_load(q + i));
-        __builtin_nontemporal_store(x, d + i);
+        put8<WT>(d + i, x);
     }
     // ragged tail (< 4 elements): an acquire, then plain 2-byte loads
     if (blockIdx.x == 0 && threadIdx.x < (len & 3)) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         const int64_t e = (n8 << 2) + threadIdx.x;
-        dst[e] = SUM ? add1<DT>(src[e], peer[e]) : src[e];
+        put2<WT>(dst + e, SUM ? add1<DT>(src[e], peer[e]) : src[e]);
     }
 }
 
@@ -199,7 +250,7 @@ __device__ __forceinline__ void stream_coherent8(const uint16_t* __restrict__ sr
 // src, peer and dst 16-byte aligned, len * 2 < 2^31): buffer loads with the
 // sc1 cache policy, which a relaxed agent-scope atomic load also uses, so
 // the data the GEMM wrote through to memory is read past this chiplet's L2.
-template <int DT, bool SUM, int kUnroll>
+template <int DT, bool SUM, int kUnroll, bool WT>
 __device__ __forceinline__ void stream_coherent16(const uint16_t* __restrict__ src,
                                                   const uint16_t* __restrict__ peer,
                                                   uint16_t* __restrict__ dst, int64_t len) {
@@ -223,28 +274,28 @@ __device__ __forceinline__ void stream_coherent16(const uint16_t* __restrict__ s
             for (int u = 0; u < kUnroll; ++u) x[u] = add8<DT>(x[u], y[u]);
         }
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) __builtin_nontemporal_store(x[u], d + i + u * stride);
+        for (int u = 0; u < kUnroll; ++u) put16<WT>(d + i + u * stride, x[u]);
     }
     for (; i < n16; i += stride) {
         u32x4_t x = bit_cast<u32x4_t>(__builtin_amdgcn_raw_buffer_load_b128(rs, (int)(i * 16), 0, kSc1));
         if constexpr (SUM) x = add8<DT>(x, __builtin_nontemporal_load(q + i));
-        __builtin_nontemporal_store(x, d + i);
+        put16<WT>(d + i, x);
     }
     // ragged tail (< 8 elements): an acquire, then plain 2-byte loads
     if (blockIdx.x == 0 && threadIdx.x < (len & 7)) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         const int64_t e = (n16 << 3) + threadIdx.x;
-        dst[e] = SUM ? add1<DT>(src[e], peer[e]) : src[e];
+        put2<WT>(dst + e, SUM ? add1<DT>(src[e], peer[e]) : src[e]);
     }
 }
 
 // Stream one segment element by element (unaligned buffers).
-template <int DT, bool SUM>
+template <int DT, bool SUM, bool WT>
 __device__ __forceinline__ void stream_elem(const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer,
                                             uint16_t* __restrict__ dst, int64_t len) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += stride)
-        dst[i] = SUM ? add1<DT>(src[i], peer[i]) : src[i];
+        put2<WT>(dst + i, SUM ? add1<DT>(src[i], peer[i]) : src[i]);
 }
 
 enum { kPathVec16 = 0, kPathCoherent8 = 1, kPathElem = 2, kPathCoherent16 = 3 };
@@ -253,45 +304,69 @@ enum { kPathVec16 = 0, kPathCoherent8 = 1, kPathElem = 2, kPathCoherent16 = 3 };
 // PATH: kPathCoherent16 / kPathCoherent8 go with SYNC == COHERENT;
 // kPathElem (unaligned buffers) waits with FENCE_ALL in every mode, since
 // plain loads follow.
-template <int DT, bool SUM, int SYNC, int PATH, int U>
+// WT: the launch counts its finished workgroups in *a.done (non-null):
+// every workgroup, written or not, writes through (put16 and friends), waits
+// until its stores are complete, and adds 1, so a wait for the grid size on
+// another stream covers the whole launch.
+template <int DT, bool SUM, int SYNC, int PATH, int U, bool WT>
 __global__ __launch_bounds__(kMaxThreads) void consume_kernel(const ConsumeArgs a) {
-    if (a.counter && !check_counter<SYNC>(a.counter, a.target, a.status)) return;
-    for (int k = 0; k < a.nseg; ++k) {
-        const ConsumeSegment g = a.seg[k];
-        const uint16_t* src = a.src + g.src_off;
-        const uint16_t* peer = SUM ? a.peer + g.src_off : nullptr;
-        uint16_t* dst = a.dst + g.dst_off;
-        if constexpr (PATH == kPathVec16) stream_vec16<DT, SUM, U>(src, peer, dst, g.len);
-        else if constexpr (PATH == kPathCoherent16) stream_coherent16<DT, SUM, U>(src, peer, dst, g.len);
-        else if constexpr (PATH == kPathCoherent8) stream_coherent8<DT, SUM, U>(src, peer, dst, g.len);
-        else stream_elem<DT, SUM>(src, peer, dst, g.len);
+    if (!a.counter || check_counter<SYNC>(a.counter, a.target, a.status)) {
+        for (int k = 0; k < a.nseg; ++k) {
+            const ConsumeSegment g = a.seg[k];
+            const uint16_t* src = a.src + g.src_off;
+            const uint16_t* peer = SUM ? a.peer + g.src_off : nullptr;
+            uint16_t* dst = a.dst + g.dst_off;
+            if constexpr (PATH == kPathVec16) stream_vec16<DT, SUM, U, WT>(src, peer, dst, g.len);
+            else if constexpr (PATH == kPathCoherent16) stream_coherent16<DT, SUM, U, WT>(src, peer, dst, g.len);
+            else if constexpr (PATH == kPathCoherent8) stream_coherent8<DT, SUM, U, WT>(src, peer, dst, g.len);
+            else stream_elem<DT, SUM, WT>(src, peer, dst, g.len);
+        }
+    }
+    if constexpr (WT) {
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        __syncthreads();
+        if (threadIdx.x == 0) __hip_atomic_fetch_add(a.done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
-template <int DT, bool SUM, int U>
+template <int DT, bool SUM, int U, bool WT>
 void launch_variant(int sync, int path, dim3 g, dim3 b, hipStream_t s, const ConsumeArgs& a) {
     if (path == kPathCoherent16)
-        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent16, U>), g, b, 0, s, a);
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent16, U, WT>), g, b, 0, s, a);
     else if (path == kPathCoherent8)
-        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent8, U>), g, b, 0, s, a);
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent8, U, WT>), g, b, 0, s, a);
     else if (path == kPathVec16 && sync == FO_SYNC_FENCE_ALL)
-        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ALL, kPathVec16, U>), g, b, 0, s, a);
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ALL, kPathVec16, U, WT>), g, b, 0, s, a);
     else if (path == kPathVec16)
-        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ONE, kPathVec16, U>), g, b, 0, s, a);
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ONE, kPathVec16, U, WT>), g, b, 0, s, a);
     else
-        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ALL, kPathElem, U>), g, b, 0, s, a);
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ALL, kPathElem, U, WT>), g, b, 0, s, a);
 }
 
+// A counting launch (a.done) always takes the full unroll: it is the last
+// group's, which runs once the GEMM is done.
 template <int DT, bool SUM>
 void launch_unroll(bool full, int sync, int path, dim3 g, dim3 b, hipStream_t s, const ConsumeArgs& a) {
-    if (full) launch_variant<DT, SUM, kUnrollFull>(sync, path, g, b, s, a);
-    else launch_variant<DT, SUM, kUnrollBeside>(sync, path, g, b, s, a);
+    if (a.done) launch_variant<DT, SUM, kUnrollFull, true>(sync, path, g, b, s, a);
+    else if (full) launch_variant<DT, SUM, kUnrollFull, false>(sync, path, g, b, s, a);
+    else launch_variant<DT, SUM, kUnrollBeside, false>(sync, path, g, b, s, a);
 }
 
 }  // namespace
 
+hipError_t launch_wait(const uint32_t* counter, uint32_t target, uint32_t* status, uint64_t timeout_ticks,
+                       hipStream_t s) {
+    hipLaunchKernelGGL(wait_kernel, dim3(1), dim3(64), 0, s, counter, target, status, timeout_ticks);
+    return hipGetLastError();
+}
+
+hipError_t launch_gate(uint32_t* gate, uint32_t tag, uint32_t* status, uint64_t timeout_ticks, hipStream_t s) {
+    hipLaunchKernelGGL(gate_kernel, dim3(1), dim3(64), 0, s, gate, tag, status, timeout_ticks);
+    return hipGetLastError();
+}
+
 hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blocks, int threads, bool full,
-                          hipStream_t s) {
+                          hipStream_t s, int* launched_blocks) {
     // The path is chosen once for the launch: every segment's pointers must
     // allow it.
     uintptr_t bits = 0;
@@ -317,6 +392,7 @@ hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blo
     if (blocks < 1) blocks = 1;
     if (blocks > max_blocks) blocks = max_blocks;
     const dim3 g((unsigned)blocks), b((unsigned)threads);
+    if (launched_blocks) *launched_blocks = (int)blocks;
     if (a.counter) {
         hipLaunchKernelGGL(wait_kernel, dim3(1), dim3(64), 0, s, a.counter, a.target, a.status, a.timeout_ticks);
         const hipError_t e = hipGetLastError();

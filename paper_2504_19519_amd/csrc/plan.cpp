@@ -497,7 +497,7 @@ const int32_t* fo_plan_group_targets(const fo_plan* p) { return p ? p->targets.d
 double fo_plan_predicted_us(const fo_plan* p) { return p ? p->predicted_us : 0.0; }
 const int32_t* fo_plan_pool_base(const fo_plan* p) { return p && !p->pool_base.empty() ? p->pool_base.data() : nullptr; }
 const int32_t* fo_plan_pool_off(const fo_plan* p) { return p && !p->pool_off.empty() ? p->pool_off.data() : nullptr; }
-int32_t fo_plan_num_counters(const fo_plan* p) { return p ? p->P + FO_DISPENSER_WORDS : 0; }
+int32_t fo_plan_num_counters(const fo_plan* p) { return p ? p->P + FO_DISPENSER_WORDS + FO_HANDOFF_WORDS : 0; }
 int32_t fo_plan_num_segments(const fo_plan* p) { return p ? (int32_t)(p->segs.size() / 5) : 0; }
 const int64_t* fo_plan_segments(const fo_plan* p) { return p ? p->segs.data() : nullptr; }
 int64_t fo_plan_dest_elems(const fo_plan* p) { return p ? p->dest_elems : 0; }

@@ -9,6 +9,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <vector>
 
 #include "consume.h"
 #include "fo_internal.h"
@@ -87,6 +88,33 @@ __global__ void fill_u32_kernel(uint32_t* p, int32_t n, uint32_t v) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n) p[i] = v;
 }
+
+// Start of an overlapped run, one workgroup on the GEMM stream: zero the
+// status word, the group and position counters (n words) and the done word,
+// make the zeros visible device-wide, then exchange the gate word for the
+// run's tag (the start handoff that the gate kernel on the consumer stream
+// waits for). If a gate of this run timed out before, the word holds the
+// tag's timed-out mark: the status word then gets bit 0 back. gate == NULL:
+// only the zeroing (a run without a consumer stream).
+__global__ __launch_bounds__(256) void reset_run_kernel(uint32_t* counters, int32_t n, uint32_t* done,
+                                                        uint32_t* status, uint32_t* gate, uint32_t tag) {
+    for (int i = threadIdx.x; i < n; i += blockDim.x) counters[i] = 0u;
+    if (threadIdx.x == 0) {
+        if (done) *done = 0u;
+        if (status) *status = 0u;
+    }
+    if (!gate) return;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint32_t old = __hip_atomic_exchange(gate, tag, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        if (old == (tag | kGateTimedOut) && status)
+            __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+// Tags of overlapped runs, unique per process (30 bits of sequence).
+std::atomic<uint32_t> g_run_seq{0};
 
 template <typename T>
 const T* dev_table(const void* dev_plan, int64_t word_off) {
@@ -337,35 +365,6 @@ fo_status fo_post_reorder(const fo_plan* plan, const void* dev_plan, const void*
     return e == hipSuccess ? FO_OK : fo::hip_fail("post-reorder launch", e);
 }
 
-namespace {
-struct EventPair {
-    int device = -1;
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-};
-thread_local EventPair t_events[8];
-
-fo_status events_for_current_device(hipEvent_t* e0, hipEvent_t* e1) {
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return fo::hip_fail("hipGetDevice", e);
-    EventPair* slot = nullptr;
-    for (auto& p : t_events) {
-        if (p.device == dev) { slot = &p; break; }
-        if (!slot && p.device < 0) slot = &p;
-    }
-    if (!slot) return fo::fail(FO_ERR_UNSUPPORTED, "too many devices used from one thread");
-    if (slot->device != dev) {
-        if ((e = hipEventCreateWithFlags(&slot->e0, hipEventDisableTiming)) != hipSuccess)
-            return fo::hip_fail("hipEventCreate", e);
-        if ((e = hipEventCreateWithFlags(&slot->e1, hipEventDisableTiming)) != hipSuccess)
-            return fo::hip_fail("hipEventCreate", e);
-        slot->device = dev;
-    }
-    *e0 = slot->e0;
-    *e1 = slot->e1;
-    return FO_OK;
-}
-}  // namespace
 
 fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const void* A, const void* W,
                             void* C_out, const void* peer, void* dst, void* out, const void* bias,
@@ -378,19 +377,30 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
     if (!dst) return fo::fail(FO_ERR_ARG, "dst is NULL");
     const bool overlap = comm_stream && comm_stream != gemm_stream;
     if (overlap && !counters) return fo::fail(FO_ERR_ARG, "an overlapped run needs counters");
+    // The null stream waits for work on other blocking streams, which would
+    // hold its reset kernel behind the gate kernel that waits for it.
+    if (overlap && !gemm_stream) return fo::fail(FO_ERR_ARG, "an overlapped run needs a created GEMM stream");
     hipStream_t s1 = (hipStream_t)gemm_stream, s2 = (hipStream_t)comm_stream;
     fo_status st;
-    if (overlap) {
-        if ((st = fo_reset_counters(counters, plan->P + FO_DISPENSER_WORDS, s1)) != FO_OK) return st;
-    }
-    if (status_word && (st = fo_reset_counters(status_word, 1, s1)) != FO_OK) return st;
-    hipEvent_t e0 = nullptr, e1 = nullptr;
     hipError_t e;
-    if (overlap) {
-        if ((st = events_for_current_device(&e0, &e1)) != FO_OK) return st;
-        if ((e = hipEventRecord(e0, s1)) != hipSuccess) return fo::hip_fail("hipEventRecord", e);
-        if ((e = hipStreamWaitEvent(s2, e0, 0)) != hipSuccess) return fo::hip_fail("hipStreamWaitEvent", e);
+    fo::ConsumeArgs a{};
+    // consume_args also yields the wait limit in device clock ticks
+    if ((st = fo::consume_args(static_cast<const uint16_t*>(C_out), static_cast<const uint16_t*>(peer),
+                               static_cast<uint16_t*>(dst), nullptr, 0, status_word, &a)) != FO_OK)
+        return st;
+    const uint64_t ticks = a.timeout_ticks;
+    // Handoff words after the group and position counters.
+    uint32_t* gate = overlap ? counters + plan->P + FO_DISPENSER_WORDS : nullptr;
+    uint32_t* done = overlap ? gate + 1 : nullptr;
+    const uint32_t tag =
+        fo::kGateTag | (fo::g_run_seq.fetch_add(1, std::memory_order_relaxed) & (fo::kGateTimedOut - 1));
+    if (overlap || status_word) {
+        hipLaunchKernelGGL(fo::reset_run_kernel, dim3(1), dim3(256), 0, s1, counters,
+                           overlap ? plan->P + FO_DISPENSER_WORDS : 0, done, status_word, gate, tag);
+        if ((e = hipGetLastError()) != hipSuccess) return fo::hip_fail("reset kernel launch", e);
     }
+    if (overlap && (e = fo::launch_gate(gate, tag, status_word, ticks, s2)) != hipSuccess)
+        return fo::hip_fail("gate kernel launch", e);
     if (gemm_begin_event && (e = hipEventRecord((hipEvent_t)gemm_begin_event, s1)) != hipSuccess)
         return fo::hip_fail("hipEventRecord", e);
     if ((st = fo_gemm_signal_reorder(plan, dev_plan, A, W, C_out, overlap ? counters : nullptr, s1)) != FO_OK)
@@ -401,33 +411,44 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
     // launch carries), as a collective library would take one call per
     // group. Groups before the last one share the device with the GEMM and
     // use the configured grid cap; the last group runs once the GEMM is
-    // done and takes the full grid.
+    // done and takes the full grid. The final launch counts its finished
+    // workgroups in the done word, for which the GEMM stream waits before
+    // the post-reorder.
     const int64_t* seg = plan->segs.data();
     const int nseg = (int)(plan->segs.size() / 5);
     const int sync = fo::g_sync_consumer.load(std::memory_order_relaxed);
     const int cap = fo::g_consumer_blocks.load(std::memory_order_relaxed);
     const int cap_threads = fo::g_consumer_threads.load(std::memory_order_relaxed);
-    fo::ConsumeArgs a{};
+    struct Launch {
+        fo::ConsumeArgs args;
+        bool last;
+    };
+    std::vector<Launch> launches;
     for (int i = 0; i < nseg;) {
         const int64_t j = seg[5 * i];
-        if ((st = fo::consume_args(static_cast<const uint16_t*>(C_out), static_cast<const uint16_t*>(peer),
-                                   static_cast<uint16_t*>(dst), overlap ? counters + j : nullptr,
-                                   (uint32_t)plan->targets[j], status_word, &a)) != FO_OK)
-            return st;
-        a.nseg = 0;
-        for (; i < nseg && seg[5 * i] == j && a.nseg < fo::kMaxConsumeSegments; ++i)
-            if (seg[5 * i + 4] > 0) a.seg[a.nseg++] = fo::ConsumeSegment{seg[5 * i + 2], seg[5 * i + 3], seg[5 * i + 4]};
-        if (a.nseg == 0) continue;
-        const bool last = j + 1 == plan->P || !overlap;
+        Launch l{a, j + 1 == plan->P || !overlap};
+        l.args.counter = overlap ? counters + j : nullptr;
+        l.args.target = (uint32_t)plan->targets[j];
+        l.args.nseg = 0;
+        for (; i < nseg && seg[5 * i] == j && l.args.nseg < fo::kMaxConsumeSegments; ++i)
+            if (seg[5 * i + 4] > 0)
+                l.args.seg[l.args.nseg++] = fo::ConsumeSegment{seg[5 * i + 2], seg[5 * i + 3], seg[5 * i + 4]};
+        if (l.args.nseg > 0) launches.push_back(l);
+    }
+    int final_blocks = 0;
+    for (size_t k = 0; k < launches.size(); ++k) {
+        fo::ConsumeArgs& c = launches[k].args;
+        const bool final_launch = overlap && k + 1 == launches.size();
+        c.done = final_launch ? done : nullptr;
+        const bool last = launches[k].last;
         const int blocks = last ? fo::kMaxConsumeBlocks : cap;
         const int threads = last ? 256 : cap_threads;
-        if ((e = fo::launch_consume(plan->dtype, sync, a, blocks, threads, last, overlap ? s2 : s1)) != hipSuccess)
+        if ((e = fo::launch_consume(plan->dtype, sync, c, blocks, threads, last, overlap ? s2 : s1,
+                                    final_launch ? &final_blocks : nullptr)) != hipSuccess)
             return fo::hip_fail("consumer launch", e);
     }
-    if (overlap) {
-        if ((e = hipEventRecord(e1, s2)) != hipSuccess) return fo::hip_fail("hipEventRecord", e);
-        if ((e = hipStreamWaitEvent(s1, e1, 0)) != hipSuccess) return fo::hip_fail("hipStreamWaitEvent", e);
-    }
+    if (final_blocks > 0 && (e = fo::launch_wait(done, (uint32_t)final_blocks, status_word, ticks, s1)) != hipSuccess)
+        return fo::hip_fail("wait kernel launch", e);
     if (out) return fo_post_reorder(plan, dev_plan, dst, out, bias, gamma, eps, do_rmsnorm, s1);
     return FO_OK;
 }

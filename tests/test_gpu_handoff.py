@@ -1,0 +1,153 @@
+"""The two device-side handoffs of an overlapped run, on the GPU.
+
+fo_run_overlapped orders its two streams without events: the reset kernel on
+the GEMM stream writes the run's tag into a gate word that a one-wave kernel
+on the consumer stream waits for (so the consumers of a run start only after
+the counters are zero and the previous run's post-reorder has read the
+destination buffer), and the final consumer launch counts its finished
+workgroups into a done word that a one-wave wait on the GEMM stream checks
+before the post-reorder (so the post-reorder reads complete groups and the
+next GEMM does not overwrite what a consumer still reads). These tests run
+back-to-back runs that share every buffer but their outputs, hold either
+stream back before a run, and force the bounded waits to time out from the
+host (a tiny wall-clock limit), which must end in the status bit and not in
+a hang.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2504_19519_amd as fo
+import workloads
+from gpu_util import dev_plan, empty16, from_dev, plan_for, say, to_dev, torch_mod, zeros_u32
+
+pytestmark = pytest.mark.gpu
+
+# workload: (M, N, K, modelled CUs, partition in waves); no RMSNorm, so every
+# output is compared bit for bit
+CASES = {
+    "rs_8192x8192x3584": (1024, 1280, 512, 8, (2, 1)),
+    "a2a_4096x7168x2048": (1024, 896, 512, 8, (1, 1, 2)),
+}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    torch = torch_mod()
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    fo.lib()
+
+
+class Setup:
+    """One small workload, its plan, two A operands and the expected output
+    of the whole path for each (the oracle's consumer and post-reorder
+    applied to the GPU's plain GEMM of that A)."""
+
+    def __init__(self, name):
+        torch = torch_mod()
+        M, N, K, cus, sizes = CASES[name]
+        w = workloads.WORKLOADS[name].with_shape(M, N, K)
+        inp = workloads.make_inputs(w)
+        self.w, self.inp = w, inp
+        self.plan, self.o = plan_for(w, inp, num_cus=cus, sizes=list(sizes))
+        self.dp = dev_plan(self.plan)
+        a0 = np.asarray(inp.A).reshape(M, K)
+        a1 = np.ascontiguousarray(a0[::-1])          # same values, other rows
+        self.A = [to_dev(a0), to_dev(a1)]
+        self.W = to_dev(inp.W)
+        self.peer = to_dev(inp.peer) if w.pattern != "subtoken" else None
+        plan_rm = fo.plan_groups(M, N, K, dtype=w.dtype, tile_m=w.tile_m, tile_n=w.tile_n,
+                                 order=w.order, num_cus=256, pattern="rowmajor", sizes=None,
+                                 curve_bytes=[1.0], curve_us=[0.0])
+        self.expected = []
+        for A in self.A:
+            C = empty16(M * N)
+            fo.gemm_signal_reorder(plan_rm, None, A, self.W, C, None)
+            torch.cuda.synchronize()
+            Cr = from_dev(C)[:M * N][oracle.reorder_index(self.o)]
+            dst = oracle.apply_consumer(self.o, Cr, inp.peer if w.pattern != "subtoken" else None, w.dtype)
+            self.expected.append(dst[oracle.post_index(self.o)])
+        self.C = empty16(M * N)
+        self.dst = empty16(self.plan.dest_elems)
+        self.counters = zeros_u32(self.plan.num_counters)
+        self.status = zeros_u32(1)
+
+    def run(self, k, out, s1, s2):
+        fo.run_overlapped(self.plan, self.dp, self.A[k % 2], self.W, self.C, self.peer, self.dst, out,
+                          counters=self.counters, status_word=self.status, gemm_stream=s1, comm_stream=s2)
+
+    def check(self, k, out):
+        n = self.w.M * self.w.N
+        np.testing.assert_array_equal(from_dev(out)[:n], self.expected[k % 2], err_msg=f"run {k}")
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_back_to_back_runs_share_buffers(name):
+    # six runs with no host synchronisation between them, alternating two A
+    # operands, share C, dst, counters and status; each writes its own out
+    torch = torch_mod()
+    say(f"[handoff back-to-back] {name}")
+    st = Setup(name)
+    outs = [empty16(st.w.M * st.w.N, st.w.dtype) for _ in range(6)]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for k, out in enumerate(outs):
+        st.run(k, out, s1, s2)
+    torch.cuda.synchronize()
+    assert int(st.status.cpu()[0]) == 0
+    for k, out in enumerate(outs):
+        st.check(k, out)
+    np.testing.assert_array_equal(st.counters.cpu().numpy()[:st.plan.P], np.array(st.o.targets))
+
+
+@pytest.mark.parametrize("held", ["gemm_stream", "comm_stream"])
+def test_a_held_stream_is_waited_for(held):
+    # a ~20 ms spin kernel on one stream ahead of the run: with the GEMM
+    # stream held, the gate holds the consumers back (they would otherwise
+    # see the previous run's counters at their targets); with the consumer
+    # stream held, the done wait holds the post-reorder back
+    torch = torch_mod()
+    say(f"[handoff held] {held}")
+    st = Setup("rs_8192x8192x3584")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    out0 = empty16(st.w.M * st.w.N, st.w.dtype)
+    st.run(0, out0, s1, s2)                 # leaves every counter at its target
+    out1 = empty16(st.w.M * st.w.N, st.w.dtype)
+    with torch.cuda.stream(s1 if held == "gemm_stream" else s2):
+        torch.cuda._sleep(50_000_000)
+    st.run(1, out1, s1, s2)
+    torch.cuda.synchronize()
+    assert int(st.status.cpu()[0]) == 0
+    st.check(0, out0)
+    st.check(1, out1)
+
+
+def test_timed_out_handoffs_raise_the_status_bit():
+    # the wall-clock limit of every wait is cut to 1 ms and the GEMM stream
+    # is held ~20 ms: the gate times out (marking the gate word), so do the
+    # consumers and the done wait; the run must end, with bit 0 of the status
+    # word set (by the reset kernel finding the mark, as the reset runs after
+    # the gate gave up). A run with the normal limit then works again on the
+    # same counters.
+    torch = torch_mod()
+    say("[handoff timeout]")
+    st = Setup("rs_8192x8192x3584")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    old = fo.get_poll_timeout_us()
+    fo.set_poll_timeout_us(1000)
+    try:
+        out0 = empty16(st.w.M * st.w.N, st.w.dtype)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s1):
+            torch.cuda._sleep(50_000_000)
+        st.run(0, out0, s1, s2)
+        torch.cuda.synchronize()
+        assert int(st.status.cpu()[0]) & 1 == 1
+    finally:
+        fo.set_poll_timeout_us(old)
+    out1 = empty16(st.w.M * st.w.N, st.w.dtype)
+    st.run(1, out1, s1, s2)
+    torch.cuda.synchronize()
+    assert int(st.status.cpu()[0]) == 0
+    st.check(1, out1)
