@@ -13,7 +13,8 @@ struct PostArgs {
     const uint16_t* gamma;      // [N] or null
     int64_t M, N;
     int32_t tile_m, tile_n, tiles_n, pattern, num_dest;
-    int32_t cpt_log2;           // log2(tile_n / 8) (a power of two for reordered patterns)
+    int32_t cpt_log2;           // log2(tile_n / 8) for reordered patterns; 31 for row-major
+                                // (a row is one piece)
     int64_t per_dest;           // SUBTILE: elements of one destination buffer
     const int32_t* tile_to_slot;
     const int32_t* dest_perm;

@@ -20,7 +20,9 @@
 //   post_norm_kernel    bias add and/or RMSNorm: the row is loaded up front
 //                       and held in registers between the sum-of-squares and
 //                       the scaling (rows up to 8192 wide, bias and gamma
-//                       copied to LDS), or read twice for wider rows.
+//                       copied to LDS), or read twice for wider rows; which
+//                       of bias, RMSNorm and gamma run is a compile-time
+//                       choice.
 // Sources are read through the caches (the consumer has just written them,
 // so part of them is still in the memory-side cache); the output is written
 // nontemporal.
@@ -115,11 +117,12 @@ __global__ __launch_bounds__(kThreads) void post_gather_kernel(const PostArgs a)
     }
 }
 
-// y = (x + bias) [* rsqrt(mean((x + bias)^2) + eps) * gamma]: bias and gamma
-// are optional (null pointers), AFFINE says whether either is present.
-template <int DT, int CH, bool AFFINE>
+// y = (x + bias) [* rsqrt(mean((x + bias)^2) + eps) * gamma]. NORM, BIAS and
+// GAMMA fix at compile time which parts run (GAMMA only with NORM), so that
+// no per-chunk branch and no value of an unused part holds registers.
+template <int DT, int CH, bool NORM, bool BIAS, bool GAMMA>
 __global__ __launch_bounds__(kThreads) void post_norm_kernel(const PostArgs a) {
-    constexpr bool kLdsAffine = AFFINE && CH > 0;
+    constexpr bool kLdsAffine = (BIAS || GAMMA) && CH > 0;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int64_t nch = a.N >> 3;
     // LDS: [bias chunks][gamma chunks] (with kLdsAffine), then the pieces
@@ -130,13 +133,10 @@ __global__ __launch_bounds__(kThreads) void post_norm_kernel(const PostArgs a) {
     const int64_t i0 = (int64_t)blockIdx.x * kRowsPerBlock;
     const u32x4_t* bias4 = reinterpret_cast<const u32x4_t*>(a.bias);
     const u32x4_t* gamma4 = reinterpret_cast<const u32x4_t*>(a.gamma);
-    const bool has_bias = AFFINE && a.bias;
-    const bool has_gamma = AFFINE && a.do_norm && a.gamma;
-    const u32x4_t zero = {0u, 0u, 0u, 0u};
     if constexpr (kLdsAffine) {
         for (int64_t c = threadIdx.x; c < nch; c += kThreads) {
-            s_bias[c] = has_bias ? bias4[c] : zero;
-            s_gamma[c] = has_gamma ? gamma4[c] : zero;
+            if constexpr (BIAS) s_bias[c] = bias4[c];
+            if constexpr (GAMMA) s_gamma[c] = gamma4[c];
         }
     }
     stage_pieces(a, bases, i0);
@@ -145,45 +145,37 @@ __global__ __launch_bounds__(kThreads) void post_norm_kernel(const PostArgs a) {
     if (i >= a.M) return;
     const lds_u32_t* rb = bases + w * a.tiles_n;
     u32x4_t* out4 = reinterpret_cast<u32x4_t*>(a.out + i * a.N);
-    auto bias_at = [&](int64_t c) -> u32x4_t {
-        if constexpr (kLdsAffine) return s_bias[c];
-        else return has_bias ? bias4[c] : zero;
-    };
-    auto gamma_at = [&](int64_t c) -> u32x4_t {
-        if constexpr (kLdsAffine) return s_gamma[c];
-        else return has_gamma ? gamma4[c] : zero;
-    };
 
-    // h = x + bias (fp32, no rounding)
-    auto shift = [&](u32x4_t xv, int64_t c, float* h) {
+    // h = x + bias (fp32, no rounding); sb: where bias chunks are read
+    auto shift = [&](u32x4_t xv, int64_t c, const lds_u32x4_t* sb, float* h) {
         widen8<DT>(xv, h);
-        if (has_bias) {
+        if constexpr (BIAS) {
             float bv[8];
-            widen8<DT>(bias_at(c), bv);
+            widen8<DT>(kLdsAffine ? sb[c] : bias4[c], bv);
 #pragma unroll
             for (int e = 0; e < 8; ++e) h[e] += bv[e];
         }
     };
-    auto sumsq = [&](u32x4_t xv, int64_t c) {
+    auto sumsq = [&](u32x4_t xv, int64_t c, const lds_u32x4_t* sb) {
         float h[8];
-        shift(xv, c, h);
-        float s = 0.0f;
+        shift(xv, c, sb, h);
+        float q = 0.0f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) s += h[e] * h[e];
-        return s;
+        for (int e = 0; e < 8; ++e) q += h[e] * h[e];
+        return q;
     };
-    auto finish = [&](int64_t c, u32x4_t xv, float inv, bool live) {
+    auto finish = [&](int64_t c, u32x4_t xv, float inv, const lds_u32x4_t* sb, const lds_u32x4_t* sg, bool live) {
         float h[8], gv[8];
-        shift(xv, c, h);
-        if (has_gamma) widen8<DT>(gamma_at(c), gv);
+        shift(xv, c, sb, h);
+        if constexpr (GAMMA) widen8<DT>(kLdsAffine ? sg[c] : gamma4[c], gv);
         u32x4_t o;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             float y0 = h[2 * e], y1 = h[2 * e + 1];
-            if (a.do_norm) {
+            if constexpr (NORM) {
                 y0 *= inv;
                 y1 *= inv;
-                if (has_gamma) {
+                if constexpr (GAMMA) {
                     y0 *= gv[2 * e];
                     y1 *= gv[2 * e + 1];
                 }
@@ -209,44 +201,56 @@ __global__ __launch_bounds__(kThreads) void post_norm_kernel(const PostArgs a) {
             xc[t] = load_chunk(a, rb, c < nch ? c : nch - 1);
         }
         float inv = 1.0f;
-        if (a.do_norm) {
+        if constexpr (NORM) {
             float ss = 0.0f;
 #pragma unroll
             for (int t = 0; t < CH; ++t) {
                 const int64_t c = lane + 64 * t;
-                const float q = sumsq(xc[t], c < nch ? c : nch - 1);
+                const float q = sumsq(xc[t], c < nch ? c : nch - 1, s_bias);
                 ss += c < nch ? q : 0.0f;
-                // bias chunks are read from LDS one at a time, not all hoisted
+                // one bias chunk at a time: the LDS reads are not all hoisted
+                // to the top, where their values would hold registers
                 if constexpr (kLdsAffine) asm volatile("" ::: "memory");
             }
             inv = rsqrt_mean(ss);
         }
-        // The scaling pass widens the stored chunks again instead of keeping
-        // the fp32 row of the first pass alive (twice the registers).
+        // The scaling pass widens the chunks again and reads bias and gamma
+        // again, through pointers the compiler cannot match with the first
+        // pass's, instead of keeping the first pass's values alive.
 #pragma unroll
         for (int t = 0; t < CH; ++t) asm volatile("" : "+v"(xc[t]));
+        // The lane index is laundered too, so that the second pass's addresses
+        // are formed here and not kept live through the first pass.
+        const lds_u32x4_t* sb = s_bias;
+        const lds_u32x4_t* sg = s_gamma;
+        int ln = lane;
+        asm volatile("" : "+v"(sb), "+v"(sg), "+v"(ln));
 #pragma unroll
         for (int t = 0; t < CH; ++t) {
-            const int64_t c = lane + 64 * t;
-            finish(c < nch ? c : nch - 1, xc[t], inv, c < nch);
+            const int64_t c = ln + 64 * t;
+            finish(c < nch ? c : nch - 1, xc[t], inv, sb, sg, c < nch);
             if constexpr (kLdsAffine) asm volatile("" ::: "memory");
         }
     } else {
         float inv = 1.0f;
-        if (a.do_norm) {
+        if constexpr (NORM) {
             float ss = 0.0f;
-            for (int64_t c = lane; c < nch; c += 64) ss += sumsq(load_chunk(a, rb, c), c);
+            for (int64_t c = lane; c < nch; c += 64) ss += sumsq(load_chunk(a, rb, c), c, s_bias);
             inv = rsqrt_mean(ss);
         }
-        for (int64_t c = lane; c < nch; c += 64) finish(c, load_chunk(a, rb, c), inv, true);
+        for (int64_t c = lane; c < nch; c += 64) finish(c, load_chunk(a, rb, c), inv, s_bias, s_gamma, true);
     }
 }
 
 template <int DT, int CH>
 void launch_norm(const PostArgs& a, dim3 g, dim3 b, hipStream_t s) {
     const size_t lds = post_lds_bytes(a);
-    if (a.bias || (a.do_norm && a.gamma)) hipLaunchKernelGGL((post_norm_kernel<DT, CH, true>), g, b, lds, s, a);
-    else hipLaunchKernelGGL((post_norm_kernel<DT, CH, false>), g, b, lds, s, a);
+    const bool bias = a.bias != nullptr, gamma = a.do_norm && a.gamma != nullptr;
+    if (!a.do_norm) hipLaunchKernelGGL((post_norm_kernel<DT, CH, false, true, false>), g, b, lds, s, a);
+    else if (bias && gamma) hipLaunchKernelGGL((post_norm_kernel<DT, CH, true, true, true>), g, b, lds, s, a);
+    else if (bias) hipLaunchKernelGGL((post_norm_kernel<DT, CH, true, true, false>), g, b, lds, s, a);
+    else if (gamma) hipLaunchKernelGGL((post_norm_kernel<DT, CH, true, false, true>), g, b, lds, s, a);
+    else hipLaunchKernelGGL((post_norm_kernel<DT, CH, true, false, false>), g, b, lds, s, a);
 }
 
 template <int DT>

@@ -342,6 +342,8 @@ fo_status fo_post_reorder(const fo_plan* plan, const void* dev_plan, const void*
             if ((1 << l) == cpt) a.cpt_log2 = l;
         if (plan->pattern != FO_PATTERN_ROWMAJOR && (plan->tile_n % 8 || a.cpt_log2 < 0))
             return fo::fail(FO_ERR_UNSUPPORTED, "post-reorder needs tile_n / 8 to be a power of two");
+        // row-major source: chunk c of a row lies at the row's first piece + c
+        if (plan->pattern == FO_PATTERN_ROWMAJOR) a.cpt_log2 = 31;
     }
     a.pattern = plan->pattern; a.num_dest = plan->num_dest;
     a.per_dest = plan->pattern == FO_PATTERN_SUBTILE

@@ -210,6 +210,40 @@ def test_post_reorder(pattern, nd, N, dtype):
     fo.post_reorder(plan, dp, dD, out, eps=1e-6, do_rmsnorm=True)
     torch.cuda.synchronize()
     assert_close_bits(from_dev(out)[:M * N], oracle.rmsnorm(x_ref, dtype, eps=1e-6), dtype, "post + RMSNorm")
+    # every combination of bias and gamma around the norm is a kernel of its own
+    fo.post_reorder(plan, dp, dD, out, bias=dB, eps=1e-6, do_rmsnorm=True)
+    torch.cuda.synchronize()
+    assert_close_bits(from_dev(out)[:M * N], oracle.rmsnorm(x_ref, dtype, bias=bias, eps=1e-6), dtype,
+                      "post + bias + RMSNorm without gamma")
+    fo.post_reorder(plan, dp, dD, out, gamma=dG, eps=1e-6, do_rmsnorm=True)
+    torch.cuda.synchronize()
+    assert_close_bits(from_dev(out)[:M * N], oracle.rmsnorm(x_ref, dtype, gamma=gamma, eps=1e-6), dtype,
+                      "post + RMSNorm with gamma, no bias")
+    # gamma without the norm is ignored: a bias-only run
+    fo.post_reorder(plan, dp, dD, out, bias=dB, gamma=dG)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(from_dev(out)[:M * N].reshape(M, N),
+                                  oracle.rmsnorm(x_ref, dtype, bias=bias, do_norm=False))
+
+
+@pytest.mark.parametrize("BN", [192, 96])
+def test_post_rowmajor_any_tile_width(BN):
+    # a row-major source is read as one piece per row, whatever tile_n / 8 is
+    torch = torch_mod()
+    M, N, BM = 512, 8 * BN, 256
+    say(f"[post rowmajor] tile_n={BN} N={N}")
+    plan = fo.plan_groups(M, N, 64, dtype="fp16", tile_m=BM, tile_n=BN, num_cus=16, pattern="rowmajor",
+                          sizes=[1])
+    src = workloads.uniform_bits(M * N, 35, "fp16", -3, 3)
+    bias = workloads.uniform_bits(N, 36, "fp16", -0.1, 0.1)
+    out = empty16(M * N, "fp16")
+    fo.post_reorder(plan, None, to_dev(src), out)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(from_dev(out)[:M * N], src)
+    fo.post_reorder(plan, None, to_dev(src), out, bias=to_dev(bias))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(from_dev(out)[:M * N].reshape(M, N),
+                                  oracle.rmsnorm(src.reshape(M, N), "fp16", bias=bias, do_norm=False))
 
 
 def test_bad_arguments_are_rejected_before_launch():
