@@ -391,7 +391,12 @@ def tile_timeline(torch, w, plan, dp, b, stream):
             "position_on_chiplet_p_mod_8": round(float(np.mean(chip == pos % 8)), 4)}
 
 
-def cpu_baseline(w, inp, seconds):
+def cpu_baseline(w, inp, seconds, sizes, num_cus):
+    """The oracle's whole path on the host: the fp64 GEMM on a seeded sample
+    of output rows (sized to about `seconds`, scaled to all rows), then the
+    plan, pre-communication reorder, consumer and post-reorder (+ bias /
+    RMSNorm) at full size on a GEMM output of the workload's shape (their
+    cost does not depend on the values). value = GEMM flops / total time."""
     import oracle
     threads = oracle.num_threads()
     rng = np.random.default_rng(w.seed + 7)
@@ -410,10 +415,33 @@ def cpu_baseline(w, inp, seconds):
     t = time.perf_counter()
     oracle.gemm_exact(inp.A, inp.W, w.dtype, rows=rows)
     dt = time.perf_counter() - t
-    flops = 2.0 * nrows * w.N * w.K
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"fp64 oracle GEMM on {nrows} of {w.M} output rows (all {w.N} columns, "
-                      f"K={w.K}), operand decode included, {dt:.1f} s"}
+    gemm_full = dt * w.M / nrows
+    stages = {"gemm_sampled_s": round(dt, 3), "gemm_all_rows_est_s": round(gemm_full, 3)}
+    t = time.perf_counter()
+    o = oracle.make_plan(w.M, w.N, w.tile_m, w.tile_n, num_cus=num_cus, order=w.order, pattern=w.pattern,
+                         num_dest=w.num_dest if w.pattern in ("subtile", "subtoken") else 0,
+                         sigma=inp.sigma, bucket=inp.bucket, sizes=tuple(int(x) for x in sizes))
+    stages["plan_s"] = time.perf_counter() - t
+    C = workloads.uniform_bits(w.M * w.N, w.seed + 8, w.dtype)
+    t = time.perf_counter()
+    Cr = C[oracle.reorder_index(o)]
+    stages["reorder_s"] = time.perf_counter() - t
+    t = time.perf_counter()
+    dst = oracle.apply_consumer(o, Cr, inp.peer if w.pattern != "subtoken" else None, w.dtype)
+    stages["consume_s"] = time.perf_counter() - t
+    t = time.perf_counter()
+    x = dst[oracle.post_index(o)].reshape(w.M, w.N)
+    if w.rmsnorm or inp.bias is not None:
+        x = oracle.rmsnorm(x, w.dtype, bias=inp.bias, gamma=inp.gamma, eps=w.eps, do_norm=w.rmsnorm)
+    stages["post_s"] = time.perf_counter() - t
+    total = gemm_full + stages["plan_s"] + stages["reorder_s"] + stages["consume_s"] + stages["post_s"]
+    for k in ("plan_s", "reorder_s", "consume_s", "post_s"):
+        stages[k] = round(stages[k], 3)
+    return {"value": w.flops / total / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"fp64 oracle GEMM on {nrows} of {w.M} output rows (all {w.N} columns, K={w.K}, "
+                      f"operand decode included, {dt:.1f} s, scaled to all rows), then the oracle's plan, "
+                      f"reorder, consumer and post-reorder at full size; {total:.1f} s per step",
+            "stages": stages}
 
 
 def main():
@@ -601,7 +629,7 @@ def main():
     cpu = None
     if not args.skip_cpu:
         log("CPU oracle baseline")
-        cpu = cpu_baseline(w, inp, args.cpu_seconds)
+        cpu = cpu_baseline(w, inp, args.cpu_seconds, plan.sizes, num_cus)
 
     plain_us, cons_all_us = res["plain_us"], res["cons_all_us"]
     gemm_tflops = flops / gemm_mean_us / 1e6
