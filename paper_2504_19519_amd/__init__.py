@@ -31,6 +31,7 @@ FP16, BF16 = 0, 1
 TILE, SUBTILE, SUBTOKEN, ROWMAJOR = 0, 1, 2, 3
 ORDER_ROWMAJOR, ORDER_GROUPED, ORDER_XCD = 0, 1, 2
 UNIT_WAVES, UNIT_TILES = 0, 1
+DISPENSER_WORDS = 8     # tile-position counters after the P group counters (FO_DISPENSER_WORDS)
 
 _DTYPES = {"fp16": FP16, "bf16": BF16, FP16: FP16, BF16: BF16}
 _PATTERNS = {"tile": TILE, "subtile": SUBTILE, "subtoken": SUBTOKEN, "rowmajor": ROWMAJOR,
@@ -143,6 +144,15 @@ def _ptr(x) -> Optional[int]:
     raise TypeError(f"cannot take a device pointer of {type(x)}")
 
 
+def _need(x, nbytes: int, what: str) -> None:
+    """A tensor argument must hold at least `nbytes` (raw pointers are taken
+    as given: the C ABI cannot see buffer sizes)."""
+    if x is not None and hasattr(x, "numel") and hasattr(x, "element_size"):
+        have = int(x.numel()) * int(x.element_size())
+        if have < nbytes:
+            raise ValueError(f"{what}: {have} bytes, the call needs {nbytes}")
+
+
 def _stream(s) -> Optional[int]:
     if s is None:
         return None
@@ -215,8 +225,9 @@ class Plan:
     def P(self) -> int: return lib().fo_plan_num_groups(self._h)
     @property
     def num_counters(self) -> int:
-        """Length of the zeroed counters array a signalling GEMM needs (P group
-        counters, then the GEMM's tile-position counters)."""
+        """Length of the counters array of a signalling run: P group counters,
+        the GEMM's tile-position counters, then the two words an overlapped run
+        uses to hand work between its streams."""
         return lib().fo_plan_num_counters(self._h)
     @property
     def sizes(self) -> np.ndarray: return self._arr(lib().fo_plan_group_sizes, self.P)
@@ -364,18 +375,29 @@ class PlanCache:
 
 
 def gemm_signal_reorder(plan: Plan, dev_plan, A, W, C_out, counters=None, stream=None) -> None:
+    _need(A, 2 * plan.M * plan.K, "A")
+    _need(W, 2 * plan.N * plan.K, "W")
+    _need(C_out, 2 * plan.M * plan.N, "C_out")
+    _need(counters, 4 * (plan.P + DISPENSER_WORDS), "counters")
     _check(lib().fo_gemm_signal_reorder(plan.handle, _ptr(dev_plan), _ptr(A), _ptr(W), _ptr(C_out),
                                         _ptr(counters), _stream(stream)))
 
 
 def consume_group(src, peer, dst, length: int, dtype, counter=None, target: int = 0,
                   status_word=None, stream=None) -> None:
+    _need(src, 2 * int(length), "src")
+    _need(peer, 2 * int(length), "peer")
+    _need(dst, 2 * int(length), "dst")
     _check(lib().fo_consume_group(_ptr(src), _ptr(peer), _ptr(dst), int(length), _DTYPES[dtype],
                                   _ptr(counter), int(target), _ptr(status_word), _stream(stream)))
 
 
 def post_reorder(plan: Plan, dev_plan, src, out, bias=None, gamma=None, eps: float = 1e-6,
                  do_rmsnorm: bool = False, stream=None) -> None:
+    _need(src, 2 * (plan.dest_elems if plan.pattern != ROWMAJOR else plan.M * plan.N), "src")
+    _need(out, 2 * plan.M * plan.N, "out")
+    _need(bias, 2 * plan.N, "bias")
+    _need(gamma, 2 * plan.N, "gamma")
     _check(lib().fo_post_reorder(plan.handle, _ptr(dev_plan), _ptr(src), _ptr(out), _ptr(bias),
                                  _ptr(gamma), float(eps), int(bool(do_rmsnorm)), _stream(stream)))
 
@@ -388,6 +410,16 @@ def run_overlapped(plan: Plan, dev_plan, A, W, C_out, peer, dst, out=None, bias=
                    eps: float = 1e-6, do_rmsnorm: bool = False, counters=None, status_word=None,
                    gemm_stream=None, comm_stream=None, gemm_begin_event=None,
                    gemm_end_event=None) -> None:
+    _need(A, 2 * plan.M * plan.K, "A")
+    _need(W, 2 * plan.N * plan.K, "W")
+    _need(C_out, 2 * plan.M * plan.N, "C_out")
+    _need(peer, 2 * plan.M * plan.N, "peer")
+    _need(dst, 2 * plan.dest_elems, "dst")
+    _need(out, 2 * plan.M * plan.N, "out")
+    _need(bias, 2 * plan.N, "bias")
+    _need(gamma, 2 * plan.N, "gamma")
+    _need(counters, 4 * plan.num_counters, "counters")
+    _need(status_word, 4, "status_word")
     _check(lib().fo_run_overlapped(plan.handle, _ptr(dev_plan), _ptr(A), _ptr(W), _ptr(C_out),
                                    _ptr(peer), _ptr(dst), _ptr(out), _ptr(bias), _ptr(gamma),
                                    float(eps), int(bool(do_rmsnorm)), _ptr(counters),

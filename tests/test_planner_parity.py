@@ -224,3 +224,22 @@ def test_counters_and_overlapped_argument_checks():
         with pytest.raises(fo.FoError) as e:
             fo.run_overlapped(p, fake, fake, fake, fake, fake, fake, None, **kw)
         assert e.value.status == -1
+
+
+def test_binding_rejects_short_tensors_before_the_call():
+    # the binding checks tensor sizes against the plan (host-side only: the
+    # tensors here are CPU tensors and the calls never reach the library)
+    import torch
+    with open(os.path.join(ROOT, "include", "fo.h")) as f:
+        m = re.search(r"#define FO_DISPENSER_WORDS (\d+)", f.read())
+    assert m and int(m.group(1)) == fo.DISPENSER_WORDS
+    p = fo.plan_groups(1024, 1024, 64, sizes=[2, 2], num_cus=8, tile_m=256, tile_n=128)
+    short = torch.zeros(p.num_counters - 1, dtype=torch.int32)
+    with pytest.raises(ValueError, match="counters"):
+        fo.run_overlapped(p, 1, 1, 1, 1, 1, 1, counters=short, gemm_stream=1, comm_stream=2)
+    with pytest.raises(ValueError, match="C_out"):
+        fo.gemm_signal_reorder(p, 1, 1, 1, torch.zeros(1024 * 1024 - 1, dtype=torch.int16))
+    with pytest.raises(ValueError, match="dst"):
+        fo.consume_group(1, None, torch.zeros(7, dtype=torch.int16), 8, "fp16")
+    with pytest.raises(ValueError, match="gamma"):
+        fo.post_reorder(p, 1, 1, 1, gamma=torch.zeros(1023, dtype=torch.int16))
