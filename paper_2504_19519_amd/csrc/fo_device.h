@@ -28,12 +28,10 @@ __device__ __forceinline__ uint32_t f32_to_f16_bits(float x) {
     return (uint32_t)bit_cast<uint16_t>((_Float16)x);
 }
 
-// fp32 -> bf16 bits, round to nearest even; NaN stays a quiet NaN.
+// fp32 -> bf16 bits, round to nearest even; NaN stays a (quiet) NaN. The
+// conversion is gfx950's v_cvt_pk_bf16_f32: no per-element branch.
 __device__ __forceinline__ uint32_t f32_to_bf16_bits(float x) {
-    uint32_t u = bit_cast<uint32_t>(x);
-    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return ((u >> 16) | 0x40u) & 0xFFFFu;
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return u >> 16;
+    return (uint32_t)bit_cast<uint16_t>((__bf16)x);
 }
 
 __device__ __forceinline__ float f16_bits_to_f32(uint32_t h) {
@@ -56,10 +54,19 @@ __device__ __forceinline__ uint32_t from_f32(float x) {
     else return f32_to_bf16_bits(x);
 }
 
-// Two fp32 values rounded and packed into one 32-bit word (low = a).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 values rounded and packed into one 32-bit word (low = a); bf16
+// pairs take one v_cvt_pk_bf16_f32.
 template <int DT>
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
-    return from_f32<DT>(a) | (from_f32<DT>(b) << 16);
+    if constexpr (DT == 0) {
+        return from_f32<DT>(a) | (from_f32<DT>(b) << 16);
+    } else {
+        const f32x2_t v = {a, b};
+        return bit_cast<uint32_t>(__builtin_convertvector(v, bf16x2_t));
+    }
 }
 
 }  // namespace fo
