@@ -377,8 +377,12 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
     if (!plan) return fo::fail(FO_ERR_ARG, "plan is NULL");
     if (plan->tiles == 0) return FO_OK;
     if (!dst) return fo::fail(FO_ERR_ARG, "dst is NULL");
-    const bool overlap = comm_stream && comm_stream != gemm_stream;
-    if (overlap && !counters) return fo::fail(FO_ERR_ARG, "an overlapped run needs counters");
+    // An overlapped run with one group has nothing to overlap (its consumer
+    // can only start once the whole GEMM is done): it runs on the GEMM stream
+    // alone, still signalling, without the stream handoffs.
+    const bool requested = comm_stream && comm_stream != gemm_stream;
+    const bool overlap = requested && plan->P > 1;
+    if (requested && !counters) return fo::fail(FO_ERR_ARG, "an overlapped run needs counters");
     // The null stream waits for work on other blocking streams, which would
     // hold its reset kernel behind the gate kernel that waits for it.
     if (overlap && !gemm_stream) return fo::fail(FO_ERR_ARG, "an overlapped run needs a created GEMM stream");
@@ -396,16 +400,16 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
     uint32_t* done = overlap ? gate + 1 : nullptr;
     const uint32_t tag =
         fo::kGateTag | (fo::g_run_seq.fetch_add(1, std::memory_order_relaxed) & (fo::kGateTimedOut - 1));
-    if (overlap || status_word) {
+    if (requested || status_word) {
         hipLaunchKernelGGL(fo::reset_run_kernel, dim3(1), dim3(256), 0, s1, counters,
-                           overlap ? plan->P + FO_DISPENSER_WORDS : 0, done, status_word, gate, tag);
+                           requested ? plan->P + FO_DISPENSER_WORDS : 0, done, status_word, gate, tag);
         if ((e = hipGetLastError()) != hipSuccess) return fo::hip_fail("reset kernel launch", e);
     }
     if (overlap && (e = fo::launch_gate(gate, tag, status_word, ticks, s2)) != hipSuccess)
         return fo::hip_fail("gate kernel launch", e);
     if (gemm_begin_event && (e = hipEventRecord((hipEvent_t)gemm_begin_event, s1)) != hipSuccess)
         return fo::hip_fail("hipEventRecord", e);
-    if ((st = fo_gemm_signal_reorder(plan, dev_plan, A, W, C_out, overlap ? counters : nullptr, s1)) != FO_OK)
+    if ((st = fo_gemm_signal_reorder(plan, dev_plan, A, W, C_out, requested ? counters : nullptr, s1)) != FO_OK)
         return st;
     if (gemm_end_event && (e = hipEventRecord((hipEvent_t)gemm_end_event, s1)) != hipSuccess)
         return fo::hip_fail("hipEventRecord", e);
