@@ -278,19 +278,22 @@ def consumer_curve(torch, w, b, stream, total_elems):
 
 
 def gemm_comm_times(torch, w, plan, dp, b, s1, s2, steps):
-    """GEMM + consume time of overlapped runs: from the GEMM's start (event
-    on the GEMM stream) to the end of the last consumer (event on the
-    communication stream); the post-reorder is not included."""
+    """GEMM + consume time of overlapped runs without the post-reorder: from
+    the GEMM's start (event on the GEMM stream) to the end of the last
+    consumer (event on the stream it ran on: the communication stream, or
+    the GEMM stream for a plan of one group, which runs serialized)."""
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
     dummy = torch.cuda.Event(enable_timing=True)
     dummy.record(s1)
+    last = s2 if plan.P > 1 else s1
     for a, c in ev:          # create the events
         a.record(s1)
-        c.record(s2)
+        c.record(last)
     for a, c in ev:
-        run_step(torch, w, plan, dp, b, s1, s2, (a, dummy))
-        c.record(s2)
+        fo.run_overlapped(plan, dp, b.A, b.W, b.C, b.peer, b.dst, None, None, None, w.eps, False,
+                          b.counters, b.status, s1, s2, a, dummy)
+        c.record(last)
     torch.cuda.synchronize()
     if int(b.status.cpu()[0]) != 0:
         raise RuntimeError("a consumer wait timed out")

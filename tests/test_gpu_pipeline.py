@@ -109,7 +109,7 @@ SMALL = {
     "ar_2048x4096x4096": (1024, 1024, 512, 8, (1, 2, 1)),
     "rs_8192x8192x3584": (1024, 1280, 512, 8, (2, 1)),          # 256x256 tiles: 20 tiles, T = 3
     "ar_rmsnorm_16384x4096x3584_bf16": (1024, 1280, 512, 8, (1, 2)),
-    "a2a_4096x7168x2048": (1024, 896, 512, 8, (1, 1, 2)),
+    "a2a_4096x7168x2048": (1024, 1280, 512, 8, (1, 2)),          # 256x256 tiles: 20 tiles, T = 3
 }
 
 
@@ -156,7 +156,7 @@ FULL = {
     "ar_2048x4096x4096": [(1,)],
     "rs_8192x8192x3584": [(1,) * 4, (2, 2), (1, 3)],
     "ar_rmsnorm_16384x4096x3584_bf16": [(1,) * 4],
-    "a2a_4096x7168x2048": [(1, 1, 1, 1)],
+    "a2a_4096x7168x2048": [(1, 1)],
 }
 
 

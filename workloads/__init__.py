@@ -95,7 +95,7 @@ WORKLOADS = {
                     "with bias add and RMSNorm over N=4096"),
     "a2a_4096x7168x2048": Workload(
         name="a2a_4096x7168x2048", M=4096, N=7168, K=2048, dtype=FP16,
-        tile_m=256, tile_n=128, order="xcd", pattern=SUBTOKEN, seed=4,
+        tile_m=256, tile_n=256, order="xcd", pattern=SUBTOKEN, seed=4,
         dist="uniform", num_dest=8, rmsnorm=True,
         description="MoE-style output projection, All-to-All stand-in: rows "
                     "go to 8 seeded buckets, restore fused with RMSNorm over "
