@@ -565,8 +565,8 @@ hipError_t launch_t(const GemmArgs& a, int grid, hipStream_t s) {
 
 hipError_t launch_gemm(int dtype, int tile_m, int tile_n, const GemmArgs& a, int grid, hipStream_t s) {
     if (tile_m == 256 && tile_n == 128)
-        return dtype == FO_FP16 ? launch_t<FO_FP16, 256, 128, 2, 2, 3, 64>(a, grid, s)
-                                : launch_t<FO_BF16, 256, 128, 2, 2, 3, 64>(a, grid, s);
+        return dtype == FO_FP16 ? launch_t<FO_FP16, 256, 128, 4, 2, 3, 64>(a, grid, s)
+                                : launch_t<FO_BF16, 256, 128, 4, 2, 3, 64>(a, grid, s);
     if (tile_m == 256 && tile_n == 256)
         return dtype == FO_FP16 ? launch_t<FO_FP16, 256, 256, 2, 4, 2, 64>(a, grid, s)
                                 : launch_t<FO_BF16, 256, 256, 2, 4, 2, 64>(a, grid, s);
