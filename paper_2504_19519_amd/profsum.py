@@ -84,10 +84,23 @@ def summarize(out_dir: str, workload: str, phase: str, sizes: str, summary: str,
                          f"{float(r['MaxNs']) / 1e3:.2f} |")
             if "gemm_signal_kernel" in k:
                 gemm_avg, gemm_name = avg, k
+    # The step phase runs warmup + timed + instrumented passes; bench.py's
+    # live GEMM figure is the average over the instrumented pass, so the
+    # trace is also averaged over the same (last) launches.
+    last_avg, last_n = None, 20
+    tpath = os.path.join(out_dir, "trace", "trace_kernel_trace.csv")
+    if gemm_name is not None and os.path.exists(tpath):
+        with open(tpath) as f:
+            d = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"])) for r in csv.DictReader(f)
+                       if _short(r["Kernel_Name"]) == gemm_name)
+        if len(d) >= last_n:
+            last_avg = sum(e - b for b, e in d[-last_n:]) / last_n / 1e3
     if live_gemm_us is not None and gemm_avg is not None:
         lines.append("")
-        lines.append(f"GEMM launch average measured by bench.py with HIP events in the same phase: "
-                     f"{live_gemm_us:.2f} us (trace: {gemm_avg:.2f} us).")
+        lines.append(f"GEMM launch average measured by bench.py with HIP events in the same phase "
+                     f"(its instrumented pass, {last_n} launches): {live_gemm_us:.2f} us; trace over the same "
+                     f"{last_n} launches: " + (f"{last_avg:.2f} us" if last_avg is not None else "n/a") +
+                     f" (all {gemm_avg:.2f} us above include warm-up).")
     vals = {p: _counter_means(os.path.join(out_dir, p, f"{p}_counter_collection.csv"))
             for p in ("step_FETCH_SIZE", "step_WRITE_SIZE", "copy_FETCH_SIZE", "copy_WRITE_SIZE")}
     copy_k = [k for k in vals["copy_FETCH_SIZE"] if "consume" in k][0]
