@@ -148,6 +148,36 @@ def test_consumer_bit_exact(dtype, length, offset, mode):
     np.testing.assert_array_equal(got, ref)
 
 
+SPECIAL_BITS = {
+    # +0, -0, smallest and largest subnormal, smallest normal, 1, -1.5, largest
+    # finite (both signs), +inf, -inf, NaN
+    "fp16": [0x0000, 0x8000, 0x0001, 0x03FF, 0x0400, 0x3C00, 0xBE00, 0x7BFF, 0xFBFF, 0x7C00, 0xFC00, 0x7E00],
+    "bf16": [0x0000, 0x8000, 0x0001, 0x007F, 0x0080, 0x3F80, 0xBFC0, 0x7F7F, 0xFF7F, 0x7F80, 0xFF80, 0x7FC0],
+}
+
+
+@pytest.mark.parametrize("dtype", ["fp16", "bf16"])
+def test_consumer_sum_special_values(dtype):
+    # every pair of special values (signed zeros, subnormals, overflow of the
+    # largest finite to infinity, inf - inf): the sum is the correctly
+    # rounded one, bit for bit; a NaN result only has to be a NaN
+    torch = torch_mod()
+    say(f"[consume special values] dtype={dtype}")
+    v = np.array(SPECIAL_BITS[dtype], dtype=np.uint16)
+    src, peer = np.repeat(v, v.size), np.tile(v, v.size)       # 144 pairs: 18 vector chunks
+    n = src.size
+    dD = empty16(n, dtype)
+    fo.consume_group(to_dev(src), to_dev(peer), dD, n, dtype)
+    torch.cuda.synchronize()
+    got = from_dev(dD)[:n]
+    ref = oracle.add_rne(src, peer, dtype)
+    exp_mask, man_mask = (0x7C00, 0x03FF) if dtype == "fp16" else (0x7F80, 0x007F)
+    nan_ref = ((ref & exp_mask) == exp_mask) & ((ref & man_mask) != 0)
+    nan_got = ((got & exp_mask) == exp_mask) & ((got & man_mask) != 0)
+    np.testing.assert_array_equal(nan_got, nan_ref)
+    np.testing.assert_array_equal(got[~nan_ref], ref[~nan_ref])
+
+
 def test_consumer_timeout_reports_and_skips():
     torch = torch_mod()
     say("[consume timeout] counter never reaches the target; 2 ms limit")
