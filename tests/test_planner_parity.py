@@ -150,6 +150,13 @@ def test_plan_errors(kwargs, status):
 def test_empty_problem():
     p = fo.plan_groups(0, 1024, 64, sizes=None, curve_bytes=[1.0], curve_us=[1.0])
     assert p.tiles == 0 and p.T == 0 and p.P == 0 and p.segments.shape == (0, 5)
+    # an empty problem launches nothing: the calls return before any device
+    # work (the pointers are never used)
+    fake = 1 << 20
+    fo.gemm_signal_reorder(p, fake, fake, fake, fake)
+    fo.post_reorder(p, fake, fake, fake)
+    fo.run_overlapped(p, fake, fake, fake, fake, fake, fake, fake, counters=fake, gemm_stream=fake,
+                      comm_stream=fake + 64)
 
 
 def test_header_symbols_are_exported():
