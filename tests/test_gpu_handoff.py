@@ -19,7 +19,7 @@ import pytest
 import oracle
 import paper_2504_19519_amd as fo
 import workloads
-from gpu_util import dev_plan, empty16, from_dev, plan_for, say, to_dev, torch_mod, zeros_u32
+from gpu_util import assert_close_bits, dev_plan, empty16, from_dev, plan_for, say, to_dev, torch_mod, zeros_u32
 
 pytestmark = pytest.mark.gpu
 
@@ -151,3 +151,50 @@ def test_timed_out_handoffs_raise_the_status_bit():
     torch.cuda.synchronize()
     assert int(st.status.cpu()[0]) == 0
     st.check(1, out1)
+
+
+def test_back_to_back_runs_at_full_size():
+    # the bench's configuration: rs 8192x8192x3584, 256 CUs, waves [1, 2, 1];
+    # three runs without host synchronisation, alternating two A operands,
+    # sharing C, dst, counters and status, each output checked bit for bit
+    # (the GPU's plain GEMM of each A is first checked against the exact
+    # product on seeded rows)
+    torch = torch_mod()
+    w = workloads.WORKLOADS["rs_8192x8192x3584"]
+    say("[handoff back-to-back full size] rs_8192x8192x3584 [1, 2, 1]")
+    inp = workloads.make_inputs(w)
+    plan, o = plan_for(w, inp, num_cus=256, sizes=[1, 2, 1])
+    dp = dev_plan(plan)
+    a0 = np.asarray(inp.A).reshape(w.M, w.K)
+    As = [to_dev(a0), to_dev(np.ascontiguousarray(a0[::-1]))]
+    Wd, peer = to_dev(inp.W), to_dev(inp.peer)
+    plan_rm = fo.plan_groups(w.M, w.N, w.K, dtype=w.dtype, tile_m=w.tile_m, tile_n=w.tile_n,
+                             order=w.order, num_cus=256, pattern="rowmajor", sizes=None,
+                             curve_bytes=[1.0], curve_us=[0.0])
+    rows = np.sort(np.random.default_rng(w.seed + 2000).choice(w.M, 8, replace=False))
+    expected = []
+    for k, A in enumerate(As):
+        C = empty16(w.M * w.N)
+        fo.gemm_signal_reorder(plan_rm, None, A, Wd, C, None)
+        torch.cuda.synchronize()
+        Cp = from_dev(C)[:w.M * w.N]
+        ak = a0 if k == 0 else np.ascontiguousarray(a0[::-1])
+        ref = oracle.encode(oracle.gemm_exact(ak, inp.W, w.dtype, rows=rows), w.dtype)
+        assert_close_bits(Cp.reshape(w.M, w.N)[rows], ref, w.dtype, "plain GEMM (sampled rows)")
+        dst = oracle.apply_consumer(o, Cp[oracle.reorder_index(o)], inp.peer, w.dtype)
+        expected.append(dst[oracle.post_index(o)])
+        del C
+    C = empty16(w.M * w.N)
+    dst = empty16(plan.dest_elems)
+    counters = zeros_u32(plan.num_counters)
+    status = zeros_u32(1)
+    outs = [empty16(w.M * w.N, w.dtype) for _ in range(3)]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for k, out in enumerate(outs):
+        fo.run_overlapped(plan, dp, As[k % 2], Wd, C, peer, dst, out, counters=counters,
+                          status_word=status, gemm_stream=s1, comm_stream=s2)
+    torch.cuda.synchronize()
+    assert int(status.cpu()[0]) == 0
+    for k, out in enumerate(outs):
+        np.testing.assert_array_equal(from_dev(out)[:w.M * w.N], expected[k % 2], err_msg=f"run {k}")
