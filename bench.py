@@ -52,7 +52,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="rs_8192x8192x3584", choices=list(workloads.WORKLOADS))
-    ap.add_argument("--phase", default="all", choices=["all", "step", "gemm", "copy", "predict", "trace"],
+    ap.add_argument("--phase", default="all",
+                    choices=["all", "step", "gemm", "copy", "predict", "trace", "slowlink"],
                     help="step/gemm/copy run only that loop (for profiler runs); predict: Algorithm 1's "
                          "estimate vs the measured GEMM+consume time of every partition")
     ap.add_argument("--sizes", default=None, help="explicit partition in waves, e.g. 1,1,2,4")
@@ -60,6 +61,8 @@ def parse():
     ap.add_argument("--consumer-grid", default=None,
                     help="grid of the consumers beside the GEMM: BLOCKSxTHREADS, e.g. 256x64")
     ap.add_argument("--serial", action="store_true", help="step phase: run the consumers on the GEMM stream")
+    ap.add_argument("--consumer-limit", type=int, default=0,
+                    help="cap every consumer launch at this many workgroups (a slower link stand-in)")
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
@@ -300,6 +303,35 @@ def gemm_comm_times(torch, w, plan, dp, b, s1, s2, steps):
     return [a.elapsed_time(c) * 1000.0 for a, c in ev]
 
 
+def slow_link_report(torch, w, inp, b, num_cus, sig_us, s1, s2):
+    """The overlap as the communication side gets slower: every consumer
+    launch capped at a few workgroups (fo_set_consumer_limit) stands in for a
+    slower interconnect. For each cap: the consumer's latency curve, the
+    partition Algorithm 1 picks on it, and overlapped vs serialized steps in
+    alternating rounds."""
+    rows = []
+    try:
+        for cap in (0, 64, 32, 16, 8):
+            fo.set_consumer_limit(cap)
+            xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N)
+            p = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys))
+            d = dev_plan(torch, p)
+            torch.cuda.synchronize()
+            ov, se = [], []
+            for _ in range(3):
+                ov.append(timed_steps(torch, w, p, d, b, s1, s2, 6, 2)[0])
+                se.append(timed_steps(torch, w, p, d, b, s1, s1, 6, 2)[0])
+            o, r = float(np.median(ov)), float(np.median(se))
+            rows.append({"consumer_limit": cap, "consume_alone_us": round(ys[-1], 2),
+                         "consume_over_gemm": round(ys[-1] / sig_us, 3),
+                         "groups": [int(x) for x in p.sizes], "predicted_us": round(p.predicted_us, 2),
+                         "overlapped_step_us": round(o, 2), "serial_step_us": round(r, 2),
+                         "speedup_vs_serial": round(r / o, 4)})
+    finally:
+        fo.set_consumer_limit(0)
+    return rows
+
+
 def partitions(T):
     """Every composition of T waves, by cut vector (bit i = cut after wave i+1)."""
     out = []
@@ -463,6 +495,8 @@ def main():
     log(f"workload {w.name}: M={w.M} N={w.N} K={w.K} {w.dtype} pattern={w.pattern}")
     if args.consumer_grid:
         fo.set_consumer_grid(*(int(x) for x in args.consumer_grid.lower().split("x")))
+    if args.consumer_limit:
+        fo.set_consumer_limit(args.consumer_limit)
     inp = workloads.make_inputs(w)
     num_cus = fo.device_num_cus(0)
     tiles = (w.M // w.tile_m) * (w.N // w.tile_n)
@@ -487,6 +521,11 @@ def main():
         return
     if args.phase == "trace":
         print(json.dumps(tile_timeline(torch, w, base_plan, dp_base, b, s1)), flush=True)
+        return
+    if args.phase == "slowlink":
+        sig = time_gemm(torch, base_plan, dp_base, b, s1, 30, 5)
+        print(json.dumps({"phase": "slowlink", "gemm_alone_us": round(sig, 2),
+                          "rows": slow_link_report(torch, w, inp, b, num_cus, sig, s1, s2)}), flush=True)
         return
     if args.phase == "predict":
         print(json.dumps(predictor_accuracy(torch, w, inp, b, base_plan, dp_base, num_cus, T, flops, s1, s2,
@@ -602,6 +641,9 @@ def main():
         grid_variants[f"{nb}x{nt}"] = {"overlapped_step_us": round(us, 2), "overlapped_gemm_us": round(gm, 2)}
     fo.set_consumer_grid(*default_grid)
 
+    # ---- a slower interconnect: every consumer launch capped ---------------
+    slow_link = slow_link_report(torch, w, inp, b, num_cus, sig_us, s1, s2) if plan.P > 0 else None
+
     # ---- consistency at full size: overlapped vs serialized output bits ----
     # (every buffer the step writes is poisoned first; 0xFFFF is a NaN)
     for buf in (b.C, b.dst, b.out):
@@ -693,6 +735,7 @@ def main():
         "sync_modes": {"default": list(default_modes), "variants": sync_variants,
                        "overlapped_equals_serial_bits": consistent},
         "consumer_grid": {"default": "%dx%d" % default_grid, "variants": grid_variants},
+        "slow_link": slow_link,
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
     }

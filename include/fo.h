@@ -342,7 +342,7 @@ fo_status fo_reset_counters(uint32_t* counters, int32_t n, void* stream);
  * group's plan segments (fo_plan_segments: 1, R or B of them). Every group
  * but the last uses the grid of fo_get_consumer_grid(); the last group,
  * which runs after the GEMM, uses up to 256 workgroups of 256 threads (as do
- * all groups of a serialized run).
+ * all groups of a serialized run); fo_set_consumer_limit caps them all.
  * With comm_stream == gemm_stream (or NULL) the same work runs serialized
  * on gemm_stream, without the handoffs and without signalling. A plan of one
  * group has nothing to overlap (its consumer can only start after the whole
@@ -403,6 +403,18 @@ void fo_get_sync_mode(int32_t* producer, int32_t* consumer);
  * Process-wide; FO_ERR_ARG outside the ranges. */
 fo_status fo_set_consumer_grid(int32_t max_blocks, int32_t threads);
 void fo_get_consumer_grid(int32_t* max_blocks, int32_t* threads);
+
+/* Cap on the workgroups of every consumer launch -- all groups of overlapped
+ * and serialized runs (the last group included) and fo_consume_group -- at
+ * max_blocks (1 .. 256); 0 = no cap (the default). A stand-in for a slower
+ * interconnect in benchmarks: the consumer's bandwidth grows with its
+ * workgroups, so a cap slows the communication side of a run without
+ * changing what it computes. Under a cap every launch uses the consumer
+ * variant that fits beside the GEMM, so that the emulated link streams at one
+ * speed in overlapped and serialized runs. Process-wide; FO_ERR_ARG outside
+ * the range. */
+fo_status fo_set_consumer_limit(int32_t max_blocks);
+int32_t fo_get_consumer_limit(void);
 
 /* Upper bound of one consumer wait, in microseconds (default 2 s; env
  * FO_POLL_TIMEOUT_US overrides at load time). */

@@ -21,7 +21,7 @@ __all__ = [
     "FoError", "Plan", "PlanCache", "plan_groups", "gemm_signal_reorder", "consume_group",
     "post_reorder", "reset_counters", "run_overlapped", "set_poll_timeout_us",
     "get_poll_timeout_us", "device_num_cus", "set_sync_mode", "get_sync_mode",
-    "set_consumer_grid", "get_consumer_grid", "set_tile_trace", "device_wall_clock_khz", "LIB_PATH",
+    "set_consumer_grid", "get_consumer_grid", "set_consumer_limit", "get_consumer_limit", "set_tile_trace", "device_wall_clock_khz", "LIB_PATH",
     "FP16", "BF16", "TILE", "SUBTILE", "SUBTOKEN", "ROWMAJOR",
 ]
 
@@ -113,6 +113,8 @@ def lib() -> ctypes.CDLL:
     L.fo_set_tile_trace.argtypes, L.fo_set_tile_trace.restype = [vp, i64], ctypes.c_int
     L.fo_device_wall_clock_khz.argtypes, L.fo_device_wall_clock_khz.restype = [pi32], ctypes.c_int
     L.fo_get_consumer_grid.argtypes = [pi32, pi32]
+    L.fo_set_consumer_limit.argtypes, L.fo_set_consumer_limit.restype = [i32], ctypes.c_int
+    L.fo_get_consumer_limit.restype = i32
     L.fo_set_poll_timeout_us.argtypes = [i64]
     L.fo_get_poll_timeout_us.restype = i64
     L.fo_device_num_cus.argtypes = [i32, pi32]
@@ -451,6 +453,16 @@ def get_consumer_grid():
     b, t = ctypes.c_int32(), ctypes.c_int32()
     lib().fo_get_consumer_grid(ctypes.byref(b), ctypes.byref(t))
     return int(b.value), int(t.value)
+
+
+def set_consumer_limit(max_blocks: int) -> None:
+    """Cap every consumer launch at `max_blocks` workgroups (0 = no cap): a
+    stand-in for a slower interconnect in benchmarks."""
+    _check(lib().fo_set_consumer_limit(int(max_blocks)))
+
+
+def get_consumer_limit() -> int:
+    return int(lib().fo_get_consumer_limit())
 
 
 def set_tile_trace(trace, capacity_tiles: int = 0) -> None:

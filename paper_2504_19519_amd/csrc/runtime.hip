@@ -54,6 +54,14 @@ std::atomic<int> g_consumer_threads{[] {
     return valid_threads(t) ? t : 256;
 }()};
 
+// Cap on the workgroups of every consumer launch (0 = none): a stand-in for
+// a slower interconnect in benchmarks (fo_set_consumer_limit).
+std::atomic<int> g_consumer_limit{0};
+int limited(int blocks) {
+    const int l = g_consumer_limit.load(std::memory_order_relaxed);
+    return l > 0 && l < blocks ? l : blocks;
+}
+
 // Tile timeline buffer of the GEMM launches (fo_set_tile_trace).
 std::atomic<uint64_t*> g_trace{nullptr};
 std::atomic<int64_t> g_trace_cap{0};
@@ -201,6 +209,16 @@ void fo_get_consumer_grid(int32_t* max_blocks, int32_t* threads) {
     if (threads) *threads = fo::g_consumer_threads.load();
 }
 
+fo_status fo_set_consumer_limit(int32_t max_blocks) {
+    fo::clear_error();
+    if (max_blocks < 0 || max_blocks > fo::kMaxConsumeBlocks)
+        return fo::fail(FO_ERR_ARG, "max_blocks must be 0 (no cap) or in [1, 256]");
+    fo::g_consumer_limit.store(max_blocks);
+    return FO_OK;
+}
+
+int32_t fo_get_consumer_limit(void) { return fo::g_consumer_limit.load(); }
+
 fo_status fo_set_tile_trace(uint64_t* trace, int64_t capacity_tiles) {
     fo::clear_error();
     if (trace && capacity_tiles < 1) return fo::fail(FO_ERR_ARG, "capacity_tiles must be >= 1");
@@ -307,7 +325,7 @@ fo_status fo_consume_group(const void* src, const void* peer, void* dst, int64_t
     a.nseg = 1;
     a.seg[0] = fo::ConsumeSegment{0, 0, len};
     hipError_t e = fo::launch_consume(dtype, fo::g_sync_consumer.load(std::memory_order_relaxed), a,
-                                      fo::g_consumer_blocks.load(std::memory_order_relaxed),
+                                      fo::limited(fo::g_consumer_blocks.load(std::memory_order_relaxed)),
                                       fo::g_consumer_threads.load(std::memory_order_relaxed), false,
                                       (hipStream_t)stream);
     return e == hipSuccess ? FO_OK : fo::hip_fail("consumer launch", e);
@@ -445,10 +463,14 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
         fo::ConsumeArgs& c = launches[k].args;
         const bool final_launch = overlap && k + 1 == launches.size();
         c.done = final_launch ? done : nullptr;
+        // Under a consumer limit every launch takes the variant that runs
+        // beside the GEMM, so that the emulated link has one speed in
+        // overlapped and serialized runs alike.
+        const bool capped = fo::g_consumer_limit.load(std::memory_order_relaxed) > 0;
         const bool last = launches[k].last;
-        const int blocks = last ? fo::kMaxConsumeBlocks : cap;
+        const int blocks = fo::limited(last ? fo::kMaxConsumeBlocks : cap);
         const int threads = last ? 256 : cap_threads;
-        if ((e = fo::launch_consume(plan->dtype, sync, c, blocks, threads, last, overlap ? s2 : s1,
+        if ((e = fo::launch_consume(plan->dtype, sync, c, blocks, threads, last && !capped, overlap ? s2 : s1,
                                     final_launch ? &final_blocks : nullptr)) != hipSuccess)
             return fo::hip_fail("consumer launch", e);
     }

@@ -185,9 +185,17 @@ def test_process_wide_settings_validate_and_round_trip():
             fo.set_sync_mode(3, 0)
         fo.set_sync_mode(1, 0)
         assert fo.get_sync_mode() == (1, 0)
+        for bad in (-1, 257):
+            with pytest.raises(fo.FoError) as e:
+                fo.set_consumer_limit(bad)
+            assert e.value.status == -1
+        assert fo.get_consumer_limit() == 0
+        fo.set_consumer_limit(16)
+        assert fo.get_consumer_limit() == 16
     finally:
         fo.set_consumer_grid(*old_grid)
         fo.set_sync_mode(*old_modes)
+        fo.set_consumer_limit(0)
 
 
 @pytest.mark.parametrize("seed", range(4))
