@@ -280,27 +280,28 @@ def consumer_curve(torch, w, b, stream, total_elems):
     return xs, ys
 
 
-def gemm_comm_times(torch, w, plan, dp, b, s1, s2, steps):
+def gemm_comm_times(torch, w, plan, dp, b, s1, s2, steps, with_gemm=False):
     """GEMM + consume time of overlapped runs without the post-reorder: from
     the GEMM's start (event on the GEMM stream) to the end of the last
     consumer (event on the stream it ran on: the communication stream, or
     the GEMM stream for a plan of one group, which runs serialized)."""
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)]
-    dummy = torch.cuda.Event(enable_timing=True)
-    dummy.record(s1)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     last = s2 if plan.P > 1 else s1
-    for a, c in ev:          # create the events
+    for a, g, c in ev:       # create the events
         a.record(s1)
+        g.record(s1)
         c.record(last)
-    for a, c in ev:
+    for a, g, c in ev:
         fo.run_overlapped(plan, dp, b.A, b.W, b.C, b.peer, b.dst, None, None, None, w.eps, False,
-                          b.counters, b.status, s1, s2, a, dummy)
+                          b.counters, b.status, s1, s2, a, g)
         c.record(last)
     torch.cuda.synchronize()
     if int(b.status.cpu()[0]) != 0:
         raise RuntimeError("a consumer wait timed out")
-    return [a.elapsed_time(c) * 1000.0 for a, c in ev]
+    if with_gemm:
+        return [a.elapsed_time(c) * 1000.0 for a, g, c in ev], [a.elapsed_time(g) * 1000.0 for a, g, c in ev]
+    return [a.elapsed_time(c) * 1000.0 for a, g, c in ev]
 
 
 def slow_link_report(torch, w, inp, b, num_cus, sig_us, s1, s2):
@@ -361,22 +362,36 @@ def predictor_accuracy(torch, w, inp, b, base_plan, dp_base, num_cus, T, flops, 
     searched = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys))
     torch.cuda.synchronize()
     meas = {c: [] for c in cands}
+    gemm_in = []
     for c in cands:                      # warm-up
         gemm_comm_times(torch, w, plans[c][0], plans[c][1], b, s1, s2, 2)
     for _ in range(5):
         for c in cands:
-            meas[c] += gemm_comm_times(torch, w, plans[c][0], plans[c][1], b, s1, s2, 4)
+            t, g = gemm_comm_times(torch, w, plans[c][0], plans[c][1], b, s1, s2, 4, with_gemm=True)
+            meas[c] += t
+            if plans[c][0].P > 1:
+                gemm_in += g
+    # the same estimate fed with the GEMM's duration inside the overlapped
+    # runs (slower than alone: the consumer's traffic), not modelled by the
+    # GEMM-alone input
+    gemm_ov = float(np.median(gemm_in)) if gemm_in else sig_us
     rows = []
     for c in cands:
         m = float(np.median(meas[c]))
         pr = plans[c][0].predicted_us
+        pr_ov = make_plan(w, inp, num_cus, sizes=c, gemm_us=gemm_ov, curve=(xs, ys)).predicted_us
         rows.append({"groups": list(c), "predicted_us": round(pr, 2), "measured_us": round(m, 2),
-                     "error_pct": round((pr - m) / m * 100, 2)})
+                     "error_pct": round((pr - m) / m * 100, 2),
+                     "predicted_overlap_gemm_us": round(pr_ov, 2),
+                     "error_overlap_gemm_pct": round((pr_ov - m) / m * 100, 2)})
     best = min(rows, key=lambda r: r["measured_us"])
     pick = next(r for r in rows if tuple(r["groups"]) == tuple(int(x) for x in searched.sizes))
     pred_best = min(rows, key=lambda r: r["predicted_us"])
     return {"phase": "predict", "workload": w.name, "waves": T, "gemm_alone_us": round(sig_us, 2),
             "mean_abs_error_pct": round(float(np.mean([abs(r["error_pct"]) for r in rows])), 2),
+            "gemm_in_overlap_us": round(gemm_ov, 2),
+            "mean_abs_error_overlap_gemm_pct":
+                round(float(np.mean([abs(r["error_overlap_gemm_pct"]) for r in rows])), 2),
             "searched_groups": pick["groups"], "searched_measured_us": pick["measured_us"],
             "best_measured_groups": best["groups"], "best_measured_us": best["measured_us"],
             "searched_over_best": round(best["measured_us"] / pick["measured_us"], 4),
