@@ -133,13 +133,19 @@ def time_gemm(torch, plan, dp, b, stream, iters, warmup, signal=True):
     return float(np.mean([a.elapsed_time(c) * 1000.0 for a, c in ev]))
 
 
+# The All-to-All stand-in moves every destination's piece of a group through
+# this one device, so Algorithm 1's estimate counts all of them (on several
+# GPUs the largest piece, the slowest link, would set the time).
+DEST_BYTES = "all"
+
+
 def make_plan(w, inp, num_cus, sizes=None, pattern=None, gemm_us=0.0, curve=None):
     pattern = pattern or w.pattern
     nd = w.num_dest if pattern in ("subtile", "subtoken") else 0
     kw = dict(dtype=w.dtype, tile_m=w.tile_m, tile_n=w.tile_n, order=w.order, num_cus=num_cus,
               pattern=pattern, num_dest=nd,
               dest_perm=inp.sigma if pattern == "subtile" else None,
-              row_bucket=inp.bucket if pattern == "subtoken" else None)
+              row_bucket=inp.bucket if pattern == "subtoken" else None, dest_bytes=DEST_BYTES)
     if sizes is not None:
         if curve is not None:      # given partition + Algorithm 1's estimate of it
             return fo.plan_groups(w.M, w.N, w.K, sizes=list(sizes), gemm_us=gemm_us, curve_bytes=curve[0],
@@ -201,7 +207,7 @@ def planner_report(w, inp, num_cus, gemm_us, curve):
     xs, ys = curve
     kw = dict(dtype=w.dtype, tile_m=w.tile_m, tile_n=w.tile_n, order=w.order, num_cus=num_cus,
               pattern=w.pattern, num_dest=w.num_dest if w.pattern in ("subtile", "subtoken") else 0,
-              dest_perm=inp.sigma if w.pattern == "subtile" else None)
+              dest_perm=inp.sigma if w.pattern == "subtile" else None, dest_bytes=DEST_BYTES)
     rng = np.random.default_rng(w.seed + 11)
 
     def bucket(M):

@@ -118,6 +118,12 @@ typedef struct {
                                  outside the samples                               */
     int32_t s_first, s_last;  /* search pruning |G_1| <= s_first, |G_P| <= s_last
                                  (Section 4.1 uses 2 and 4); <= 0 means no bound    */
+    int32_t all_dest_bytes;   /* SUBTOKEN data size of a group in the estimate:
+                                 0 = its largest per-destination piece (the slowest
+                                 link of a real All-to-All, Section 4.2: maximum
+                                 across GPUs); 1 = all its pieces (one device moves
+                                 every piece, as the one-GPU stand-in consumer
+                                 does). Other patterns ignore it.                  */
 } fo_grouping;
 
 typedef struct fo_plan fo_plan;   /* opaque, library-owned host memory */

@@ -441,19 +441,21 @@ def make_plan(M: int, N: int, BM: int, BN: int, *, num_cus: int, wg_per_cu: int 
     return plan
 
 
-def slot_range_bytes(plan: Plan, f0: int, f1: int, elem_bytes: int = 2) -> int:
+def slot_range_bytes(plan: Plan, f0: int, f1: int, elem_bytes: int = 2, all_dest: bool = False) -> int:
     """Data a group owning slots [f0, f1) hands to the communication
     (Algorithm 1, get_data_size). For the All-to-All pattern the largest
     per-destination piece stands in for the slowest destination (Section 4.2:
-    the maximum across GPUs is taken for the imbalanced All-to-All)."""
-    if plan.pattern == SUBTOKEN:
+    the maximum across GPUs is taken for the imbalanced All-to-All); with
+    ``all_dest`` every piece counts (one device moving all of them, which is
+    what a one-GPU stand-in of the exchange does)."""
+    if plan.pattern == SUBTOKEN and not all_dest:
         return int(max(plan.pool_base[f1, b] - plan.pool_base[f0, b]
                        for b in range(plan.num_dest))) * plan.BN * elem_bytes
     return (f1 - f0) * plan.BM * plan.BN * elem_bytes
 
 
 def search_partition(plan: Plan, gemm_us: float, curve_bytes, curve_us,
-                     s_first: int = 2, s_last: int = 4, elem_bytes: int = 2):
+                     s_first: int = 2, s_last: int = 4, elem_bytes: int = 2, all_dest: bool = False):
     """Algorithm 1 on a plan's geometry (its waves, tiles and pools; its own
     partition is ignored). Returns (partition in waves, predicted us)."""
     T = plan.T
@@ -461,7 +463,7 @@ def search_partition(plan: Plan, gemm_us: float, curve_bytes, curve_us,
     def comm_for(sizes):
         first = group_first_slots(sizes, "waves", plan.W, plan.tiles)
         lat = [interp_latency(curve_bytes, curve_us,
-                              slot_range_bytes(plan, first[j], first[j + 1], elem_bytes))
+                              slot_range_bytes(plan, first[j], first[j + 1], elem_bytes, all_dest))
                for j in range(len(sizes))]
         return lambda j: lat[j]
 

@@ -63,7 +63,8 @@ class _Grouping(ctypes.Structure):
                 ("sizes", ctypes.POINTER(ctypes.c_int32)), ("gemm_us", ctypes.c_double),
                 ("curve_bytes", ctypes.POINTER(ctypes.c_double)),
                 ("curve_us", ctypes.POINTER(ctypes.c_double)), ("curve_len", ctypes.c_int32),
-                ("s_first", ctypes.c_int32), ("s_last", ctypes.c_int32)]
+                ("s_first", ctypes.c_int32), ("s_last", ctypes.c_int32),
+                ("all_dest_bytes", ctypes.c_int32)]
 
 
 _lib = None
@@ -287,8 +288,11 @@ def _problem(M: int, N: int, K: int, *, dtype="fp16", tile_m: int = 256, tile_n:
     return prob, (perm, buck)
 
 
+_DEST_BYTES = {"largest": 0, "all": 1}
+
+
 def _grouping(sizes: Optional[Sequence[int]] = None, unit="waves", gemm_us: float = 0.0,
-              curve_bytes=None, curve_us=None, s_first: int = 2, s_last: int = 4):
+              curve_bytes=None, curve_us=None, s_first: int = 2, s_last: int = 4, dest_bytes: str = "largest"):
     """An fo_grouping and the arrays it points to."""
     sz = _i32_array(sizes)
     cb, cu = _f64_array(curve_bytes), _f64_array(curve_us)
@@ -298,7 +302,7 @@ def _grouping(sizes: Optional[Sequence[int]] = None, unit="waves", gemm_us: floa
                     curve_bytes=ctypes.cast(cb, ctypes.POINTER(ctypes.c_double)) if cb is not None else None,
                     curve_us=ctypes.cast(cu, ctypes.POINTER(ctypes.c_double)) if cu is not None else None,
                     curve_len=0 if curve_bytes is None else len(curve_bytes),
-                    s_first=s_first, s_last=s_last)
+                    s_first=s_first, s_last=s_last, all_dest_bytes=_DEST_BYTES[dest_bytes])
     return grp, (sz, cb, cu)
 
 
@@ -321,8 +325,9 @@ def plan_groups(M: int, N: int, K: int, **kw) -> Plan:
     """fo_plan_groups. Keywords: the fo_problem fields (dtype, tile_m, tile_n,
     order, group_m, num_xcds, num_cus, wg_per_cu, reserved_cus, pattern,
     num_dest, dest_perm, row_bucket) and the fo_grouping ones (sizes, unit,
-    gemm_us, curve_bytes, curve_us, s_first, s_last); sizes=None runs the
-    Algorithm 1 search (needs gemm_us and the latency curve)."""
+    gemm_us, curve_bytes, curve_us, s_first, s_last, dest_bytes = "largest" or
+    "all": an All-to-All group's data size in the estimate); sizes=None runs
+    the Algorithm 1 search (needs gemm_us and the latency curve)."""
     L = lib()
     prob_kw, grp_kw = _split(kw)
     prob, keep_p = _problem(M, N, K, **prob_kw)
@@ -357,11 +362,14 @@ class PlanCache:
         _check(lib().fo_plan_cache_add(self._h, ctypes.byref(prob), ctypes.byref(grp)))
 
     def lookup(self, M: int, N: int, K: int, **kw):
-        """fo_plan_cache_lookup: (Plan, M of the entry used)."""
-        prob, keep_p = _problem(M, N, K, **kw)
+        """fo_plan_cache_lookup: (Plan, M of the entry used). Takes the
+        problem keywords of plan_groups (grouping keywords are ignored: the
+        partition comes from the cache)."""
+        prob_kw, _ = _split(kw)
+        prob, keep_p = _problem(M, N, K, **prob_kw)
         out, matched = ctypes.c_void_p(), ctypes.c_int64()
         _check(lib().fo_plan_cache_lookup(self._h, ctypes.byref(prob), ctypes.byref(out), ctypes.byref(matched)))
-        return _plan_of(out.value, M, N, K, kw), int(matched.value)
+        return _plan_of(out.value, M, N, K, prob_kw), int(matched.value)
 
     def __len__(self) -> int:
         return int(lib().fo_plan_cache_size(self._h))

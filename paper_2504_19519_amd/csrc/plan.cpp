@@ -44,10 +44,11 @@ void firsts_from_waves(const std::vector<int32_t>& sizes, int32_t W, int32_t til
 }
 
 // Bytes handed to the communication by slots [f0, f1) (Algorithm 1,
-// get_data_size); All-to-All takes its largest per-destination piece.
-double range_bytes(const fo_plan& p, int32_t f0, int32_t f1) {
+// get_data_size); All-to-All takes its largest per-destination piece unless
+// all_dest (then every piece of the group counts).
+double range_bytes(const fo_plan& p, int32_t f0, int32_t f1, bool all_dest) {
     const double eb = fo::dtype_bytes(p.dtype);
-    if (p.pattern == FO_PATTERN_SUBTOKEN) {
+    if (p.pattern == FO_PATTERN_SUBTOKEN && !all_dest) {
         int64_t mx = 0;
         for (int b = 0; b < p.num_dest; ++b) {
             const int64_t n = (int64_t)p.pool_base[(size_t)f1 * p.num_dest + b] -
@@ -66,7 +67,7 @@ double predict(const fo_plan& p, const std::vector<int32_t>& sizes, double gemm_
     double acc_p = 0.0, acc_m = 0.0;
     auto comm = [&](size_t j) {
         return interp_latency(g.curve_bytes, g.curve_us, g.curve_len,
-                              range_bytes(p, first_scratch[j], first_scratch[j + 1]));
+                              range_bytes(p, first_scratch[j], first_scratch[j + 1], g.all_dest_bytes != 0));
     };
     for (size_t i = 0; i < sizes.size(); ++i) {
         const double t_m = i > 0 ? comm(i - 1) : 0.0;
@@ -84,6 +85,7 @@ fo_status check_curve(const fo_grouping& g) {
             return fo::fail(FO_ERR_ARG, "curve bytes must be positive and ascending, latencies >= 0");
     }
     if (!(g.gemm_us >= 0.0)) return fo::fail(FO_ERR_ARG, "gemm_us must be >= 0");
+    if (g.all_dest_bytes != 0 && g.all_dest_bytes != 1) return fo::fail(FO_ERR_ARG, "all_dest_bytes must be 0 or 1");
     return FO_OK;
 }
 

@@ -9,6 +9,7 @@ import itertools
 import json
 import os
 
+import numpy as np
 import pytest
 
 import oracle
@@ -231,3 +232,24 @@ def test_interp_latency():
     assert oracle.interp_latency(xs, ys, 800.0) == pytest.approx(4.0)   # end-point bandwidth
     assert oracle.interp_latency(xs, ys, 50.0) == pytest.approx(0.5)
     assert oracle.interp_latency(xs, ys, 0.0) == 0.0
+
+
+@pytest.mark.parametrize("B", [1, 3, 8])
+def test_all_to_all_group_bytes(B):
+    # every tile row goes to exactly one destination pool, so a group's pieces
+    # add up to its tiles' bytes; the largest piece is at most that, equal
+    # with one destination, and at least the average over destinations
+    rng = np.random.default_rng(60 + B)
+    M, N, BM, BN = 1024, 512, 256, 128                      # 16 tiles
+    bucket = rng.integers(0, B, M)
+    o = oracle.make_plan(M, N, BM, BN, num_cus=4, order="xcd", pattern="subtoken", num_dest=B,
+                         bucket=bucket, sizes=(1, 2, 1))
+    first = o.first
+    for j in range(len(first) - 1):
+        f0, f1 = first[j], first[j + 1]
+        total = oracle.slot_range_bytes(o, f0, f1, 2, all_dest=True)
+        largest = oracle.slot_range_bytes(o, f0, f1, 2)
+        assert total == (f1 - f0) * BM * BN * 2
+        assert largest <= total and largest * B >= total
+        if B == 1:
+            assert largest == total

@@ -106,7 +106,8 @@ def _curve(seed):
 
 @pytest.mark.parametrize("seed", range(6))
 @pytest.mark.parametrize("pattern,nd", [("tile", 0), ("subtoken", 8), ("subtile", 4)])
-def test_predictive_search_matches_oracle(seed, pattern, nd):
+@pytest.mark.parametrize("dest_bytes", ["largest", "all"])
+def test_predictive_search_matches_oracle(seed, pattern, nd, dest_bytes):
     rng = np.random.default_rng(100 + seed)
     M, N, BM, BN = 4096, 7168, 256, 128      # 896 tiles, 3.5 waves at 256 CUs
     cus = int(rng.choice([64, 128, 256]))
@@ -116,10 +117,10 @@ def test_predictive_search_matches_oracle(seed, pattern, nd):
     sigma = rng.permutation(nd) if pattern == "subtile" else None
     p = fo.plan_groups(M, N, 2048, num_cus=cus, pattern=pattern, num_dest=nd, row_bucket=bucket,
                        dest_perm=sigma, sizes=None, gemm_us=gemm_us, curve_bytes=xs, curve_us=ys,
-                       s_first=2, s_last=4)
+                       s_first=2, s_last=4, dest_bytes=dest_bytes)
     o = oracle.make_plan(M, N, BM, BN, num_cus=cus, order="xcd", pattern=pattern, num_dest=nd,
                          bucket=bucket, sigma=sigma, sizes=(-(-896 // cus),))
-    best, t = oracle.search_partition(o, gemm_us, xs, ys, 2, 4)
+    best, t = oracle.search_partition(o, gemm_us, xs, ys, 2, 4, all_dest=dest_bytes == "all")
     assert tuple(p.sizes) == best
     assert p.predicted_us == pytest.approx(t, rel=1e-12)
 
