@@ -257,3 +257,21 @@ def test_plan_from_cache_runs_the_path(name):
     o = oracle.make_plan(w.M, w.N, w.tile_m, w.tile_n, num_cus=cus, order=w.order, pattern=w.pattern,
                          num_dest=nd, sigma=inp.sigma, bucket=inp.bucket, sizes=sizes, unit="waves")
     check(w, inp, plan, o)
+
+
+@pytest.mark.parametrize("limit", [8, 1])
+@pytest.mark.parametrize("name", ["rs_8192x8192x3584", "a2a_4096x7168x2048"])
+def test_capped_consumers_give_the_same_bits(name, limit):
+    # a consumer launch cap (the slower-link stand-in) changes grids and the
+    # consumer variant of every launch, not the result
+    old = fo.get_consumer_limit()
+    fo.set_consumer_limit(limit)
+    try:
+        M, N, K, cus, sizes = SMALL[name]
+        w = workloads.WORKLOADS[name].with_shape(M, N, K)
+        say(f"[capped consumers] limit={limit} {w.name}")
+        inp = workloads.make_inputs(w)
+        plan, o = plan_for(w, inp, num_cus=cus, sizes=list(sizes))
+        check(w, inp, plan, o)
+    finally:
+        fo.set_consumer_limit(old)
