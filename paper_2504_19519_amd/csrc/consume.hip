@@ -346,11 +346,12 @@ void launch_variant(int sync, int path, dim3 g, dim3 b, hipStream_t s, const Con
         hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ALL, kPathElem, U, WT>), g, b, 0, s, a);
 }
 
-// A counting launch (a.done) always takes the full unroll: it is the last
-// group's, which runs once the GEMM is done.
+// A counting launch (a.done) is the last group's; it takes the unroll its
+// `full` flag asks for like any other launch.
 template <int DT, bool SUM>
 void launch_unroll(bool full, int sync, int path, dim3 g, dim3 b, hipStream_t s, const ConsumeArgs& a) {
-    if (a.done) launch_variant<DT, SUM, kUnrollFull, true>(sync, path, g, b, s, a);
+    if (a.done && full) launch_variant<DT, SUM, kUnrollFull, true>(sync, path, g, b, s, a);
+    else if (a.done) launch_variant<DT, SUM, kUnrollBeside, true>(sync, path, g, b, s, a);
     else if (full) launch_variant<DT, SUM, kUnrollFull, false>(sync, path, g, b, s, a);
     else launch_variant<DT, SUM, kUnrollBeside, false>(sync, path, g, b, s, a);
 }
