@@ -198,3 +198,25 @@ def test_back_to_back_runs_at_full_size():
     assert int(status.cpu()[0]) == 0
     for k, out in enumerate(outs):
         np.testing.assert_array_equal(from_dev(out)[:w.M * w.N], expected[k % 2], err_msg=f"run {k}")
+
+
+def test_two_plans_alternate_on_the_same_streams():
+    # two workloads (ReduceScatter and All-to-All shapes), each with its own
+    # buffers and counters, run alternately on one pair of streams without
+    # host synchronisation, as consecutive layers would: every output is the
+    # one its own plan expects
+    torch = torch_mod()
+    say("[handoff two plans alternating]")
+    a, b = Setup("rs_8192x8192x3584"), Setup("a2a_4096x7168x2048")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = []
+    torch.cuda.synchronize()
+    for k in range(6):
+        st = a if k % 2 == 0 else b
+        out = empty16(st.w.M * st.w.N, st.w.dtype)
+        st.run(k // 2, out, s1, s2)
+        outs.append((st, k // 2, out))
+    torch.cuda.synchronize()
+    assert int(a.status.cpu()[0]) == 0 and int(b.status.cpu()[0]) == 0
+    for st, k, out in outs:
+        st.check(k, out)
