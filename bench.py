@@ -6,25 +6,29 @@ counter reset -> signalling, reordering GEMM on stream 1 || per-group
 consumers on stream 2 -> post-reorder (fused bias / RMSNorm when the workload
 has them). Inputs are resident in HBM before the timed region starts.
 
-Default workload: fp16 GEMM M=8192, N=8192, K=3584 (MLP down-projection
+Headline workload: fp16 GEMM M=8192, N=8192, K=3584 (MLP down-projection
 shard), 256x256 tiles (4 waves on 256 CUs), ReduceScatter stand-in (R=4)
 with the group partition chosen by the planner's predictive search from the
 measured GEMM time and consumer latency curve.
 
-Prints one JSON line. `value` is whole-step throughput (GEMM flops per step
-time); `roofline` is the GEMM kernel itself (its launches timed with HIP
-events inside the timed steps); the other fields report the plain GEMM, the
-interference of the reorder + signal epilogue, the consumer's and the
-post-reorder's HBM bandwidth, serialized vs overlapped time and the
-group-size sweep. `cpu_baseline` times the CPU oracle's GEMM on a bounded
-sample of output rows.
+Prints one JSON line. `value` is whole-step throughput (GEMM flops / time of
+the whole step: GEMM, consumers and post-reorder); `roofline` is the GEMM
+kernel itself (its launches timed with HIP events on the GEMM's stream inside
+overlapped steps). Further keys: the GEMM alone with the plain row-major
+epilogue (static schedule, and the same position dispensers, coherent stores
+and counters as the signalling runs), the overhead of each reorder pattern
+(Section 6.6, Table 5: GEMM epilogue and fused post-reorder + RMSNorm), the
+consumer's and the post-reorder's HBM bandwidth, overlapped vs serialized
+steps, the fraction of the theoretical speedup (Section 6.4), Algorithm 1's
+estimate against measurement, the group-size sweep at two tile shapes, every
+other workload's summary, and `cpu_baseline` (the oracle's whole path on a
+bounded sample).
 """
 from __future__ import annotations
 
 import argparse
 import dataclasses
 import json
-import math
 import os
 import sys
 import time
@@ -40,6 +44,12 @@ import workloads  # noqa: E402
 METRIC = "signaled+reordered fp16 GEMM TFLOP/s (% MFMA peak); overlap speedup vs serial"
 PEAK_TFLOPS = 256 * 2.4e9 * 4096 / 1e12      # dense fp16/bf16 MFMA: 2516.6 TFLOP/s
 PEAK_HBM_GBS = 8000.0
+HEADLINE = "rs_8192x8192x3584"
+OTHER_WORKLOADS = ("tiny", "ar_2048x4096x4096", "ar_rmsnorm_16384x4096x3584_bf16", "a2a_4096x7168x2048")
+
+# Options of every library call of this run (None: the process defaults); the
+# slow-link phase sets a consumer launch cap here.
+OPTS = None
 
 
 def log(msg):
@@ -51,25 +61,26 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="rs_8192x8192x3584", choices=list(workloads.WORKLOADS))
+    ap.add_argument("--workload", default=HEADLINE, choices=list(workloads.WORKLOADS))
     ap.add_argument("--phase", default="all",
-                    choices=["all", "step", "gemm", "copy", "predict", "trace", "slowlink"],
+                    choices=["all", "step", "gemm", "copy", "predict", "trace", "slowlink", "sync"],
                     help="step/gemm/copy run only that loop (for profiler runs); predict: Algorithm 1's "
-                         "estimate vs the measured GEMM+consume time of every partition")
+                         "estimate vs the measured GEMM+consume time of every partition, at the workload's "
+                         "size and at M/4, M/2 and 2M; trace: tile timeline; slowlink: consumer launch caps; "
+                         "sync: the producer/consumer publication modes")
     ap.add_argument("--sizes", default=None, help="explicit partition in waves, e.g. 1,1,2,4")
-    ap.add_argument("--tile", default=None, help="override the workload's output tile, e.g. 256x256")
+    ap.add_argument("--tile", default=None, help="override the workload's output tile, e.g. 256x128")
     ap.add_argument("--consumer-grid", default=None,
                     help="grid of the consumers beside the GEMM: BLOCKSxTHREADS, e.g. 256x64")
     ap.add_argument("--serial", action="store_true", help="step phase: run the consumers on the GEMM stream")
-    ap.add_argument("--consumer-limit", type=int, default=0,
-                    help="cap every consumer launch at this many workgroups (a slower link stand-in)")
     ap.add_argument("--skip-cpu", action="store_true")
+    ap.add_argument("--skip-workloads", action="store_true", help="headline workload only")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
 
 
 class Bufs:
-    def __init__(self, torch, w, inp, plans):
+    def __init__(self, torch, w, inp, dest_elems):
         dev = "cuda"
 
         def d(bits):
@@ -80,9 +91,8 @@ class Bufs:
         self.bias = d(inp.bias) if inp.bias is not None else None
         self.gamma = d(inp.gamma) if inp.gamma is not None else None
         n = w.M * w.N
-        dest = max(p.dest_elems for p in plans)
         self.C = torch.empty(n, dtype=torch.int16, device=dev)
-        self.dst = torch.empty(dest, dtype=torch.int16, device=dev)
+        self.dst = torch.empty(max(dest_elems, n), dtype=torch.int16, device=dev)
         self.out = torch.empty(n, dtype=torch.int16, device=dev)
         self.counters = torch.zeros(64, dtype=torch.int32, device=dev)
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
@@ -92,6 +102,11 @@ def dev_plan(torch, plan):
     buf = torch.empty(plan.device_bytes // 4 + 4, dtype=torch.int32, device="cuda")
     plan.to_device(buf)
     return buf
+
+
+def check_status(b, what):
+    if int(b.status.cpu()[0]) != 0:
+        raise RuntimeError(f"a device-side wait timed out during {what}")
 
 
 def time_loop(torch, fn, iters, warmup, stream):
@@ -107,11 +122,12 @@ def time_loop(torch, fn, iters, warmup, stream):
     return e0.elapsed_time(e1) * 1000.0 / iters      # us per iteration
 
 
-def time_gemm(torch, plan, dp, b, stream, iters, warmup, signal=True):
+def time_gemm(torch, plan, dp, b, stream, iters, warmup, signal=True, opts=None):
     """Mean time of one GEMM launch (us), each bracketed by its own event
-    pair; with signal=True the counters (group counters and the GEMM's
-    tile-position counters) are zeroed before every launch, outside the
-    events."""
+    pair; with signal=True the group counters are zeroed before every launch
+    (outside the events) and the GEMM signals them, taking its positions from
+    the dispensers; signal=False: no counters (static schedule, plain
+    stores)."""
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(iters)]
 
@@ -120,7 +136,8 @@ def time_gemm(torch, plan, dp, b, stream, iters, warmup, signal=True):
             fo.reset_counters(b.counters, plan.num_counters, stream)
         if pair:
             pair[0].record(stream)
-        fo.gemm_signal_reorder(plan, dp, b.A, b.W, b.C, b.counters if signal else None, stream)
+        fo.gemm_signal_reorder(plan, dp, b.A, b.W, b.C, b.counters if signal else None, stream,
+                               opts=opts if opts is not None else OPTS)
         if pair:
             pair[1].record(stream)
 
@@ -139,13 +156,21 @@ def time_gemm(torch, plan, dp, b, stream, iters, warmup, signal=True):
 DEST_BYTES = "all"
 
 
-def make_plan(w, inp, num_cus, sizes=None, pattern=None, gemm_us=0.0, curve=None):
+def make_plan(w, inp, num_cus, sizes=None, pattern=None, gemm_us=0.0, curve=None, bucket=None):
+    """The plan of workload w (or of another reorder pattern on its shape:
+    R = 4 identity destinations for subtile, B = 8 buckets from `bucket` for
+    subtoken)."""
     pattern = pattern or w.pattern
-    nd = w.num_dest if pattern in ("subtile", "subtoken") else 0
+    if pattern == w.pattern:
+        nd = w.num_dest if pattern in ("subtile", "subtoken") else 0
+        sigma = inp.sigma if pattern == "subtile" else None
+        bucket = inp.bucket if pattern == "subtoken" and bucket is None else bucket
+    else:
+        nd = {"subtile": 4, "subtoken": 8}.get(pattern, 0)
+        sigma = None
     kw = dict(dtype=w.dtype, tile_m=w.tile_m, tile_n=w.tile_n, order=w.order, num_cus=num_cus,
-              pattern=pattern, num_dest=nd,
-              dest_perm=inp.sigma if pattern == "subtile" else None,
-              row_bucket=inp.bucket if pattern == "subtoken" else None, dest_bytes=DEST_BYTES)
+              pattern=pattern, num_dest=nd, dest_perm=sigma,
+              row_bucket=bucket if pattern == "subtoken" else None, dest_bytes=DEST_BYTES)
     if sizes is not None:
         if curve is not None:      # given partition + Algorithm 1's estimate of it
             return fo.plan_groups(w.M, w.N, w.K, sizes=list(sizes), gemm_us=gemm_us, curve_bytes=curve[0],
@@ -161,7 +186,7 @@ def make_plan(w, inp, num_cus, sizes=None, pattern=None, gemm_us=0.0, curve=None
 def run_step(torch, w, plan, dp, b, s1, s2, ev=None):
     fo.run_overlapped(plan, dp, b.A, b.W, b.C, b.peer, b.dst, b.out, b.bias, b.gamma, w.eps,
                       w.rmsnorm, b.counters, b.status, s1, s2,
-                      ev[0] if ev else None, ev[1] if ev else None)
+                      ev[0] if ev else None, ev[1] if ev else None, opts=OPTS)
 
 
 def timed_steps(torch, w, plan, dp, b, s1, s2, steps, warmup):
@@ -187,16 +212,252 @@ def timed_steps(torch, w, plan, dp, b, s1, s2, steps, warmup):
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     step_us = t0.elapsed_time(t1) * 1000.0 / steps
-    if int(b.status.cpu()[0]) != 0:
-        raise RuntimeError("a consumer wait timed out during the timed steps")
+    check_status(b, "the timed steps")
     for k in range(steps):
         run_step(torch, w, plan, dp, b, s1, s2, ev[k])
     torch.cuda.synchronize()
     gemm = [a.elapsed_time(c) * 1000.0 for a, c in ev]
-    if int(b.status.cpu()[0]) != 0:
-        raise RuntimeError("a consumer wait timed out during the instrumented steps")
+    check_status(b, "the instrumented steps")
     return step_us, float(np.mean(gemm)), float(np.median(gemm)), wall
 
+
+def traffic_bytes(w):
+    """HBM bytes per GEMM launch (FETCH_SIZE + WRITE_SIZE, scaled by a plain
+    copy of known size) from the committed rocprofv3 summary of this
+    workload's overlapped steps; None if there is none or the GEMM has
+    changed since it was taken."""
+    from paper_2504_19519_amd import profsum
+    t = profsum.read_traffic(os.path.join(ROOT, "profiles", f"gemm_step_{w.name}.md"), w.name)
+    return None if t is None else round(t)
+
+
+def consume_all(torch, w, b, stream, n, iters, warmup):
+    """The consumer over the whole buffer in one launch on the full grid (how
+    the last group of an overlapped run streams)."""
+    full = fo.options(consumer_blocks=256, consumer_threads=256)
+    if OPTS is not None:
+        full.consumer_limit = OPTS.consumer_limit
+    return time_loop(torch, lambda: fo.consume_group(b.C, b.peer, b.dst, n, w.dtype, None, 0, None, stream,
+                                                     opts=full), iters, warmup, stream)
+
+
+def consumer_curve(torch, w, b, stream, total_elems):
+    """Consumer latency vs bytes (one launch, no wait, the grid the consumers
+    beside the GEMM use): the 1-GPU stand-in for the communication bandwidth
+    curve the search interpolates."""
+    xs, ys = [], []
+    n = 1 << 15
+    while n <= total_elems:
+        us = time_loop(torch, lambda: fo.consume_group(b.C, b.peer, b.dst, n, w.dtype, None, 0, None, stream,
+                                                       opts=OPTS), 20, 3, stream)
+        xs.append(2.0 * n)
+        ys.append(us)
+        if n == total_elems:
+            break
+        n = min(n * 2, total_elems)
+    return xs, ys
+
+
+def gemm_comm_times(torch, w, plan, dp, b, s1, s2, steps, with_gemm=False):
+    """GEMM + consume time of overlapped runs without the post-reorder: from
+    the GEMM's start (event on the GEMM stream) to the end of the last
+    consumer (event on the stream it ran on: the communication stream, or
+    the GEMM stream for a plan of one group, which runs serialized)."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    last = s2 if plan.P > 1 else s1
+    for a, g, c in ev:       # create the events
+        a.record(s1)
+        g.record(s1)
+        c.record(last)
+    for a, g, c in ev:
+        fo.run_overlapped(plan, dp, b.A, b.W, b.C, b.peer, b.dst, None, None, None, w.eps, False,
+                          b.counters, b.status, s1, s2, a, g, opts=OPTS)
+        c.record(last)
+    torch.cuda.synchronize()
+    check_status(b, "GEMM + consume runs")
+    if with_gemm:
+        return [a.elapsed_time(c) * 1000.0 for a, g, c in ev], [a.elapsed_time(g) * 1000.0 for a, g, c in ev]
+    return [a.elapsed_time(c) * 1000.0 for a, g, c in ev]
+
+
+def theoretical(plan, sig_us, cons_all_us, post_us):
+    """Lower bound of an overlapped step (Section 6.4: the communication of
+    the last group cannot be hidden, nor that of the first group before its
+    compute is done): the GEMM plus the last group's share of the consumer,
+    or the first group's compute plus the whole consumer, plus the
+    post-reorder."""
+    tiles = int(sum(plan.targets))
+    last_share = plan.targets[-1] / tiles
+    first = sig_us * plan.targets[0] / tiles
+    return max(sig_us + cons_all_us * last_share, first + cons_all_us) + post_us
+
+
+def overlap_rounds(torch, w, plan, dp, base_plan, dp_base, b, s1, s2, rounds, per):
+    """Overlapped and serialized steps, GEMM + consume of the overlapped run,
+    the GEMM alone and the consumer alone (whole buffer, full grid), in
+    alternating rounds so that all see the same device state (clock,
+    temperature)."""
+    ov, se, ov_g, se_g, gc, ga, ca = [], [], [], [], [], [], []
+    n_all = w.M * w.N
+    for _ in range(rounds):
+        us, gm, _, _ = timed_steps(torch, w, plan, dp, b, s1, s2, per, 2)
+        ov.append(us)
+        ov_g.append(gm)
+        us, gm, _, _ = timed_steps(torch, w, plan, dp, b, s1, s1, per, 2)
+        se.append(us)
+        se_g.append(gm)
+        gc.append(float(np.median(gemm_comm_times(torch, w, plan, dp, b, s1, s2, per))))
+        ga.append(time_gemm(torch, base_plan, dp_base, b, s1, per, 1))
+        ca.append(consume_all(torch, w, b, s1, n_all, per, 1))
+    med = lambda v: float(np.median(v))  # noqa: E731
+    return {"overlapped_step_us": med(ov), "serial_step_us": med(se), "overlapped_rounds_us": ov,
+            "serial_rounds_us": se, "gemm_in_overlapped_us": med(ov_g), "gemm_in_serial_us": med(se_g),
+            "gemm_consume_overlapped_us": med(gc), "gemm_alone_us": med(ga), "consume_alone_us": med(ca)}
+
+
+def overlap_fields(r, bound_us):
+    """Derived overlap figures: speedup over the serialized step, GEMM +
+    consume against max(GEMM, consume), and the fractions of the theoretical
+    bound (Section 6.4: achieved over theoretical speedup, and bound over
+    achieved time)."""
+    ov, se = r["overlapped_step_us"], r["serial_step_us"]
+    th_speedup = se / bound_us
+    return {
+        "overlapped_step_us": round(ov, 2), "serial_step_us": round(se, 2),
+        "speedup_vs_serial": round(se / ov, 4),
+        "gemm_consume_overlapped_us": round(r["gemm_consume_overlapped_us"], 2),
+        "gemm_alone_us": round(r["gemm_alone_us"], 2), "consume_alone_us": round(r["consume_alone_us"], 2),
+        "overlapped_gemm_consume_over_max": round(r["gemm_consume_overlapped_us"] /
+                                                  max(r["gemm_alone_us"], r["consume_alone_us"]), 4),
+        "gemm_in_overlapped_us": round(r["gemm_in_overlapped_us"], 2),
+        "gemm_in_serial_us": round(r["gemm_in_serial_us"], 2),
+        "theoretical_bound_us": round(bound_us, 2), "theoretical_speedup": round(th_speedup, 4),
+        "fraction_of_theoretical_speedup": round((se / ov - 1) / (th_speedup - 1), 4) if th_speedup > 1 else None,
+        "fraction_of_theoretical_performance": round(bound_us / ov, 4),
+    }
+
+
+def with_bucket_seed(w):
+    """A seeded row-to-bucket map for the subtoken pattern on a workload that
+    has none (the Table 5 analogue on the headline shape)."""
+    return np.random.default_rng(w.seed + 5).integers(0, 8, w.M).astype(np.int32)
+
+
+def table5(torch, w, inp, b, num_cus, T, s1, rounds=3, iters=30):
+    """Section 6.6, Table 5 analogue on this workload's shape: the GEMM with
+    each reorder pattern's epilogue against the row-major epilogue, all
+    signalling counters under the same position dispensers and coherent
+    stores (interleaved rounds), and the fused post-reorder + RMSNorm of each
+    pattern against the same kernel on the identity map; the plain gather
+    (no norm) beside it."""
+    bucket = with_bucket_seed(w)
+    plans = {p: make_plan(w, inp, num_cus, sizes=[1] * T, pattern=p, bucket=bucket)
+             for p in ("rowmajor", "tile", "subtile", "subtoken")}
+    dps = {p: dev_plan(torch, q) for p, q in plans.items()}
+    torch.cuda.synchronize()
+    gemm = {p: [] for p in plans}
+    static = []
+    for _ in range(rounds):
+        static.append(time_gemm(torch, plans["rowmajor"], dps["rowmajor"], b, s1, iters, 3, signal=False))
+        for p in plans:
+            gemm[p].append(time_gemm(torch, plans[p], dps[p], b, s1, iters, 3))
+    g = {p: float(np.median(v)) for p, v in gemm.items()}
+    st = float(np.median(static))
+    n = w.M * w.N
+    b.dst[:n].copy_(b.C[:n])        # finite values to normalise
+    post = {}
+    for norm in (False, True):
+        ident = time_loop(torch, lambda: fo.post_reorder(plans["rowmajor"], None, b.dst, b.out, None, None, w.eps,
+                                                         norm, s1), iters, 5, s1)
+        post[norm] = {"identity_us": round(ident, 2)}
+        for p in ("tile", "subtile", "subtoken"):
+            us = time_loop(torch, lambda: fo.post_reorder(plans[p], dps[p], b.dst, b.out, None, None, w.eps, norm,
+                                                          s1), iters, 5, s1)
+            post[norm][p] = {"us": round(us, 2), "overhead_pct": round((us / ident - 1) * 100, 2)}
+    rows = {p: {"us": round(g[p], 2), "overhead_pct": round((g[p] / g["rowmajor"] - 1) * 100, 2)}
+            for p in ("tile", "subtile", "subtoken")}
+    return {"shape": [w.M, w.N, w.K], "tile": [w.tile_m, w.tile_n],
+            "gemm_rowmajor_signalled_us": round(g["rowmajor"], 2), "gemm_rowmajor_static_us": round(st, 2),
+            "gemm_epilogue": rows,
+            "post_reorder_rmsnorm": post[True], "post_reorder_gather": post[False],
+            "paper_context": "A800 / RTX 4090: GEMM +0.07-0.68 %, fused RMSNorm +7.46-9.63 % (Table 5)"}
+
+
+def sweep(torch, w, inp, num_cus, b, s1, s2, steps):
+    """Group-size sweep (waves per group, Section 6.5) on the workload's tile
+    and on 256x128 tiles (twice the waves), overlapped steps; sizes above the
+    wave count are listed as skipped."""
+    res = {}
+    for tm, tn in sorted({(w.tile_m, w.tile_n), (256, 128)}, reverse=True):
+        wt = dataclasses.replace(w, tile_m=tm, tile_n=tn)
+        T = -(-((w.M // tm) * (w.N // tn)) // num_cus)
+        rows, skipped = {}, []
+        base = make_plan(wt, inp, num_cus, sizes=[1] * T)
+        dbase = dev_plan(torch, base)
+        torch.cuda.synchronize()
+        alone = time_gemm(torch, base, dbase, b, s1, 20, 3)
+        for g in (w.sweep or (1, 2, 4, 8)):
+            if g > T:
+                skipped.append(g)
+                continue
+            sizes = [g] * (T // g) + ([T % g] if T % g else [])
+            p = make_plan(wt, inp, num_cus, sizes=sizes)
+            d = dev_plan(torch, p)
+            torch.cuda.synchronize()
+            us, gm, _, _ = timed_steps(torch, wt, p, d, b, s1, s2, steps, 3)
+            rows[str(g)] = {"groups": sizes, "step_us": round(us, 2), "gemm_us": round(gm, 2)}
+        res[f"{tm}x{tn}"] = {"waves": T, "gemm_alone_us": round(alone, 2), "waves_per_group": rows,
+                             "skipped_waves_per_group": skipped}
+    return res
+
+
+def workload_summary(torch, name, num_cus, steps):
+    """One workload end to end: GEMM alone, consumer and post-reorder
+    bandwidth, the Algorithm 1 plan, overlapped vs serialized steps and the
+    overlap fractions."""
+    w = workloads.WORKLOADS[name]
+    log(f"workload {name}")
+    inp = workloads.make_inputs(w)
+    tiles = (w.M // w.tile_m) * (w.N // w.tile_n)
+    T = -(-tiles // num_cus)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    if w.groups is not None:
+        base_plan = make_plan(w, inp, num_cus, sizes=list(w.groups)) if w.group_unit == "waves" else \
+            fo.plan_groups(w.M, w.N, w.K, dtype=w.dtype, tile_m=w.tile_m, tile_n=w.tile_n, order=w.order,
+                           num_cus=num_cus, pattern=w.pattern, sizes=list(w.groups), unit=w.group_unit)
+    else:
+        base_plan = make_plan(w, inp, num_cus, sizes=[1] * T)
+    b = Bufs(torch, w, inp, base_plan.dest_elems)
+    dp_base = dev_plan(torch, base_plan)
+    torch.cuda.synchronize()
+    sig_us = time_gemm(torch, base_plan, dp_base, b, s1, 30, 5)
+    xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N)
+    if w.groups is not None:
+        plan, dp = base_plan, dp_base
+    else:
+        plan = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys))
+        dp = dev_plan(torch, plan)
+    torch.cuda.synchronize()
+    r = overlap_rounds(torch, w, plan, dp, base_plan, dp_base, b, s1, s2, 3, max(6, steps // 4))
+    post_us = time_loop(torch, lambda: fo.post_reorder(plan, dp, b.dst, b.out, b.bias, b.gamma, w.eps, w.rmsnorm,
+                                                       s1), 30, 5, s1)
+    n = w.M * w.N
+    cons_bytes = (6 if b.peer is not None else 4) * n
+    post_bytes = 4.0 * n + (2.0 * w.N * (int(w.bias) + int(w.gamma)))
+    bound = theoretical(plan, r["gemm_alone_us"], r["consume_alone_us"], post_us)
+    g_in = r["gemm_in_overlapped_us"]
+    return {"M": w.M, "N": w.N, "K": w.K, "dtype": w.dtype, "pattern": w.pattern, "tile": [w.tile_m, w.tile_n],
+            "waves": T, "groups": [int(x) for x in plan.sizes], "unit": w.group_unit,
+            "gemm_alone_us": round(sig_us, 2), "gemm_tflops": round(w.flops / sig_us / 1e6, 2),
+            "gemm_frac_peak": round(w.flops / sig_us / 1e6 / PEAK_TFLOPS, 4),
+            "gemm_in_step_tflops": round(w.flops / g_in / 1e6, 2),
+            "consumer_GBps": round(cons_bytes / r["consume_alone_us"] / 1e3, 1),
+            "consumer_frac_hbm": round(cons_bytes / r["consume_alone_us"] / 1e3 / PEAK_HBM_GBS, 4),
+            "post_reorder_us": round(post_us, 2), "post_reorder_GBps": round(post_bytes / post_us / 1e3, 1),
+            "post_reorder_frac_hbm": round(post_bytes / post_us / 1e3 / PEAK_HBM_GBS, 4),
+            "step_tflops": round(w.flops / r["overlapped_step_us"] / 1e6, 2),
+            "overlap": overlap_fields(r, bound)}
 
 def planner_report(w, inp, num_cus, gemm_us, curve):
     """Host cost of the planner's online stage (Section 4.2): Algorithm 1 on
@@ -247,96 +508,6 @@ def planner_report(w, inp, num_cus, gemm_us, curve):
                        "estimate_cached_over_searched": round(est / best.predicted_us, 4)})
     return {"search_us": round(search_us, 1), "cache_lookup_us": round(lookup_us, 1),
             "cached_sizes_M": reps_m, "unseen": unseen}
-
-
-def traffic_bytes(w):
-    """HBM bytes per GEMM launch (FETCH_SIZE + WRITE_SIZE, scaled by a plain
-    copy of known size) from the committed rocprofv3 summary of this
-    workload's overlapped steps; None if there is none or the GEMM has
-    changed since it was taken."""
-    from paper_2504_19519_amd import profsum
-    t = profsum.read_traffic(os.path.join(ROOT, "profiles", f"gemm_step_{w.name}.md"), w.name)
-    return None if t is None else round(t)
-
-
-def with_grid(grid, fn):
-    """Run fn() with the consumer grid set to `grid` (blocks, threads)."""
-    old = fo.get_consumer_grid()
-    fo.set_consumer_grid(*grid)
-    try:
-        return fn()
-    finally:
-        fo.set_consumer_grid(*old)
-
-
-def consumer_curve(torch, w, b, stream, total_elems):
-    """Consumer latency vs bytes (one launch, no wait, the grid the consumers
-    beside the GEMM use): the 1-GPU stand-in for the communication bandwidth
-    curve the search interpolates."""
-    xs, ys = [], []
-    n = 1 << 15
-    while n <= total_elems:
-        us = time_loop(torch, lambda: fo.consume_group(b.C, b.peer, b.dst, n, w.dtype, None, 0, None, stream),
-                       20, 3, stream)
-        xs.append(2.0 * n)
-        ys.append(us)
-        if n == total_elems:
-            break
-        n = min(n * 2, total_elems)
-    return xs, ys
-
-
-def gemm_comm_times(torch, w, plan, dp, b, s1, s2, steps, with_gemm=False):
-    """GEMM + consume time of overlapped runs without the post-reorder: from
-    the GEMM's start (event on the GEMM stream) to the end of the last
-    consumer (event on the stream it ran on: the communication stream, or
-    the GEMM stream for a plan of one group, which runs serialized)."""
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-           torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    last = s2 if plan.P > 1 else s1
-    for a, g, c in ev:       # create the events
-        a.record(s1)
-        g.record(s1)
-        c.record(last)
-    for a, g, c in ev:
-        fo.run_overlapped(plan, dp, b.A, b.W, b.C, b.peer, b.dst, None, None, None, w.eps, False,
-                          b.counters, b.status, s1, s2, a, g)
-        c.record(last)
-    torch.cuda.synchronize()
-    if int(b.status.cpu()[0]) != 0:
-        raise RuntimeError("a consumer wait timed out")
-    if with_gemm:
-        return [a.elapsed_time(c) * 1000.0 for a, g, c in ev], [a.elapsed_time(g) * 1000.0 for a, g, c in ev]
-    return [a.elapsed_time(c) * 1000.0 for a, g, c in ev]
-
-
-def slow_link_report(torch, w, inp, b, num_cus, sig_us, s1, s2):
-    """The overlap as the communication side gets slower: every consumer
-    launch capped at a few workgroups (fo_set_consumer_limit) stands in for a
-    slower interconnect. For each cap: the consumer's latency curve, the
-    partition Algorithm 1 picks on it, and overlapped vs serialized steps in
-    alternating rounds."""
-    rows = []
-    try:
-        for cap in (0, 64, 32, 16, 8):
-            fo.set_consumer_limit(cap)
-            xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N)
-            p = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys))
-            d = dev_plan(torch, p)
-            torch.cuda.synchronize()
-            ov, se = [], []
-            for _ in range(3):
-                ov.append(timed_steps(torch, w, p, d, b, s1, s2, 6, 2)[0])
-                se.append(timed_steps(torch, w, p, d, b, s1, s1, 6, 2)[0])
-            o, r = float(np.median(ov)), float(np.median(se))
-            rows.append({"consumer_limit": cap, "consume_alone_us": round(ys[-1], 2),
-                         "consume_over_gemm": round(ys[-1] / sig_us, 3),
-                         "groups": [int(x) for x in p.sizes], "predicted_us": round(p.predicted_us, 2),
-                         "overlapped_step_us": round(o, 2), "serial_step_us": round(r, 2),
-                         "speedup_vs_serial": round(r / o, 4)})
-    finally:
-        fo.set_consumer_limit(0)
-    return rows
 
 
 def partitions(T):
@@ -412,11 +583,8 @@ def tile_timeline(torch, w, plan, dp, b, stream):
     tiles = plan.tiles
     trace = torch.zeros(4 * tiles, dtype=torch.int64, device="cuda")
     time_gemm(torch, plan, dp, b, stream, 10, 5)
-    fo.set_tile_trace(trace, tiles)
-    try:
-        time_gemm(torch, plan, dp, b, stream, 1, 0)
-    finally:
-        fo.set_tile_trace(None)
+    time_gemm(torch, plan, dp, b, stream, 1, 0,
+              opts=fo.options(tile_trace=trace, tile_trace_capacity=tiles))
     khz = fo.device_wall_clock_khz()
     t = trace.cpu().numpy().reshape(-1, 4)
     us = 1000.0 / khz
@@ -500,7 +668,95 @@ def cpu_baseline(w, inp, seconds, sizes, num_cus):
             "stages": stages}
 
 
+def slow_link(torch, w, inp, b, base_plan, dp_base, num_cus, s1, s2):
+    """The overlap as the communication side gets slower: every consumer
+    launch capped at a few workgroups (the consumer_limit option) stands in
+    for a slower interconnect. For each cap: the consumer's latency curve, the
+    partition Algorithm 1 picks on it, and overlapped vs serialized steps in
+    alternating rounds."""
+    global OPTS
+    rows = []
+    sig_us = time_gemm(torch, base_plan, dp_base, b, s1, 30, 5)
+    try:
+        for cap in (0, 64, 32, 16, 8):
+            OPTS = fo.options(consumer_limit=cap)
+            xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N)
+            p = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys))
+            d = dev_plan(torch, p)
+            torch.cuda.synchronize()
+            ov, se = [], []
+            for _ in range(3):
+                ov.append(timed_steps(torch, w, p, d, b, s1, s2, 6, 2)[0])
+                se.append(timed_steps(torch, w, p, d, b, s1, s1, 6, 2)[0])
+            o, r = float(np.median(ov)), float(np.median(se))
+            rows.append({"consumer_limit": cap, "consume_alone_us": round(ys[-1], 2),
+                         "consume_over_gemm": round(ys[-1] / sig_us, 3),
+                         "groups": [int(x) for x in p.sizes], "predicted_us": round(p.predicted_us, 2),
+                         "overlapped_step_us": round(o, 2), "serial_step_us": round(r, 2),
+                         "speedup_vs_serial": round(r / o, 4)})
+    finally:
+        OPTS = None
+    return rows
+
+
+def sync_modes(torch, w, inp, b, base_plan, dp_base, num_cus, s1, s2):
+    """The three publication schemes of a finished tile (producer, consumer
+    modes), the GEMM alone and the overlapped step with each."""
+    global OPTS
+    sig_us = time_gemm(torch, base_plan, dp_base, b, s1, 30, 5)
+    xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N)
+    plan = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys))
+    dp = dev_plan(torch, plan)
+    torch.cuda.synchronize()
+    rows = {}
+    try:
+        for pm, cm in ((0, 0), (1, 1), (2, 2)):
+            OPTS = fo.options(sync_producer=pm, sync_consumer=cm)
+            sg = time_gemm(torch, base_plan, dp_base, b, s1, 30, 5)
+            us, gm, _, _ = timed_steps(torch, w, plan, dp, b, s1, s2, 20, 3)
+            rows[f"{pm}{cm}"] = {"signaled_alone_us": round(sg, 2), "overlapped_step_us": round(us, 2),
+                                 "overlapped_gemm_us": round(gm, 2)}
+    finally:
+        OPTS = None
+    return rows
+
+
+def predictor_breadth(torch, w, num_cus, steps):
+    """Algorithm 1's estimate against measurement over every partition at the
+    workload's size and at M/4, M/2 and 2M (the sizes a plan cache of the
+    family would hold; Section 6.5, Fig. 14 analogue)."""
+    rows, per_size = [], []
+    for frac in (1, 2, 4, 8):
+        M = w.M * frac // 4
+        if M % w.tile_m or M <= 0:
+            continue
+        ws = w.with_shape(M, w.N, w.K)
+        inp = workloads.make_inputs(ws)
+        tiles = (ws.M // ws.tile_m) * (ws.N // ws.tile_n)
+        T = -(-tiles // num_cus)
+        s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+        base_plan = make_plan(ws, inp, num_cus, sizes=[1] * T)
+        b = Bufs(torch, ws, inp, base_plan.dest_elems)
+        dp_base = dev_plan(torch, base_plan)
+        torch.cuda.synchronize()
+        log(f"predict {ws.name}: T={T}")
+        r = predictor_accuracy(torch, ws, inp, b, base_plan, dp_base, num_cus, T, ws.flops, s1, s2, None)
+        per_size.append({k: v for k, v in r.items() if k not in ("phase", "partitions")})
+        rows += [dict(p, M=M) for p in r["partitions"]]
+        del b
+        torch.cuda.empty_cache()
+    errs = [abs(p["error_pct"]) for p in rows]
+    errs_ov = [abs(p["error_overlap_gemm_pct"]) for p in rows]
+    return {"phase": "predict", "workload": w.name, "combinations": len(rows),
+            "mean_abs_error_pct": round(float(np.mean(errs)), 2),
+            "mean_abs_error_overlap_gemm_pct": round(float(np.mean(errs_ov)), 2),
+            "searched_over_best_min": round(min(s["searched_over_best"] for s in per_size), 4),
+            "searched_over_best_mean": round(float(np.mean([s["searched_over_best"] for s in per_size])), 4),
+            "sizes": per_size, "partitions": rows}
+
+
 def main():
+    global OPTS
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
@@ -516,18 +772,19 @@ def main():
     log(f"workload {w.name}: M={w.M} N={w.N} K={w.K} {w.dtype} pattern={w.pattern}")
     if args.consumer_grid:
         fo.set_consumer_grid(*(int(x) for x in args.consumer_grid.lower().split("x")))
-    if args.consumer_limit:
-        fo.set_consumer_limit(args.consumer_limit)
-    inp = workloads.make_inputs(w)
     num_cus = fo.device_num_cus(0)
+    if args.phase == "predict":
+        print(json.dumps(predictor_breadth(torch, w, num_cus, args.steps)), flush=True)
+        return
+    inp = workloads.make_inputs(w)
     tiles = (w.M // w.tile_m) * (w.N // w.tile_n)
     T = -(-tiles // num_cus)
     flops = w.flops
     s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
 
-    plan_rm = make_plan(w, inp, num_cus, pattern="rowmajor")
+    plan_rm = make_plan(w, inp, num_cus, sizes=[1] * T, pattern="rowmajor")
     base_plan = make_plan(w, inp, num_cus, sizes=[1] * T)
-    b = Bufs(torch, w, inp, [plan_rm, base_plan])
+    b = Bufs(torch, w, inp, base_plan.dest_elems)
     dp_rm = dev_plan(torch, plan_rm)
     dp_base = dev_plan(torch, base_plan)
     torch.cuda.synchronize()
@@ -535,30 +792,18 @@ def main():
     if args.phase == "copy":
         # plain copy of a known size: calibration run for the HBM byte counters
         n = w.M * w.N
-        us = with_grid((256, 256), lambda: time_loop(
-            torch, lambda: fo.consume_group(b.C, None, b.dst, n, w.dtype, None, 0, None, s1),
-            args.steps, args.warmup, s1))
+        us = time_loop(torch, lambda: fo.consume_group(b.C, None, b.dst, n, w.dtype, None, 0, None, s1,
+                                                       opts={"consumer_blocks": 256, "consumer_threads": 256}),
+                       args.steps, args.warmup, s1)
         print(json.dumps({"phase": "copy", "bytes_read": 2 * n, "bytes_written": 2 * n, "us": us}))
         return
     if args.phase == "trace":
         print(json.dumps(tile_timeline(torch, w, base_plan, dp_base, b, s1)), flush=True)
         return
-    if args.phase == "slowlink":
-        sig = time_gemm(torch, base_plan, dp_base, b, s1, 30, 5)
-        print(json.dumps({"phase": "slowlink", "gemm_alone_us": round(sig, 2),
-                          "rows": slow_link_report(torch, w, inp, b, num_cus, sig, s1, s2)}), flush=True)
-        return
-    if args.phase == "predict":
-        print(json.dumps(predictor_accuracy(torch, w, inp, b, base_plan, dp_base, num_cus, T, flops, s1, s2,
-                                            args)), flush=True)
-        return
     if args.phase == "gemm":
         us = time_gemm(torch, base_plan, dp_base, b, s1, args.steps, args.warmup)
         print(json.dumps({"phase": "gemm", "us": us, "tflops": flops / us / 1e6}))
         return
-
-    # ---- components alone ------------------------------------------------
-    res = {}
     if args.phase == "step":
         # profiler run: only identical overlapped steps (one group per wave
         # unless --sizes), so per-kernel averages match the live timing
@@ -573,20 +818,28 @@ def main():
                           "consumer_grid": list(fo.get_consumer_grid()), "step_us": round(step_us, 2),
                           "gemm_us": round(gemm_mean_us, 2), "gemm_tflops": round(flops / gemm_mean_us / 1e6, 2)}))
         return
-    if args.phase == "all":
-        log("plain GEMM / signaled GEMM")
-        plain_us = time_gemm(torch, plan_rm, None, b, s1, 100, 10, signal=False)
-        sig_us = time_gemm(torch, base_plan, dp_base, b, s1, 100, 10)
-        log("consumer curve")
-        n_all = w.M * w.N
-        xs, ys = consumer_curve(torch, w, b, s1, n_all)
-        cons_bytes_per_elem = 6 if b.peer is not None else 4
-        # whole buffer on the full grid (how the last group runs)
-        cons_all_us = with_grid((256, 256), lambda: time_loop(
-            torch, lambda: fo.consume_group(b.C, b.peer, b.dst, n_all, w.dtype, None, 0, None, s1), 20, 3, s1))
-        res.update(cons_gentle_us=ys[-1])
-        res.update(plain_us=plain_us, sig_us=sig_us, cons_all_us=cons_all_us,
-                   cons_gbs=cons_bytes_per_elem * n_all / cons_all_us / 1e3, curve=(xs, ys))
+    if args.phase == "slowlink":
+        print(json.dumps({"phase": "slowlink", "rows": slow_link(torch, w, inp, b, base_plan, dp_base, num_cus,
+                                                                  s1, s2)}), flush=True)
+        return
+    if args.phase == "sync":
+        print(json.dumps({"phase": "sync", "rows": sync_modes(torch, w, inp, b, base_plan, dp_base, num_cus, s1,
+                                                              s2)}), flush=True)
+        return
+
+    # ---- GEMM alone: plain (static schedule / signalled) vs reordered ------
+    log("GEMM alone: row-major static, row-major signalled, reordered signalled")
+    plain_static, plain_sig, sig = [], [], []
+    for _ in range(3):
+        plain_static.append(time_gemm(torch, plan_rm, dp_rm, b, s1, 30, 5, signal=False))
+        plain_sig.append(time_gemm(torch, plan_rm, dp_rm, b, s1, 30, 5))
+        sig.append(time_gemm(torch, base_plan, dp_base, b, s1, 30, 5))
+    plain_static_us, plain_sig_us, sig_us = (float(np.median(v)) for v in (plain_static, plain_sig, sig))
+    log("consumer curve")
+    n_all = w.M * w.N
+    xs, ys = consumer_curve(torch, w, b, s1, n_all)
+    cons_bytes_per_elem = 6 if b.peer is not None else 4
+    cons_all_us = consume_all(torch, w, b, s1, n_all, 20, 3)
 
     # ---- the plan: explicit, or Algorithm 1 on the measured inputs ---------
     if args.sizes:
@@ -598,72 +851,15 @@ def main():
     log(f"plan: T={plan.T} groups={list(plan.sizes)} predicted {plan.predicted_us:.1f} us")
     planner = planner_report(w, inp, num_cus, sig_us, (xs, ys)) if not args.sizes else None
 
-    # ---- timed steps -----------------------------------------------------
-    # overlapped vs serialized, in alternating rounds so that both see the
-    # same device state (clock, temperature)
+    # ---- overlapped vs serialized, alternating rounds ----------------------
     log("overlapped vs serialized rounds")
-    rounds, per = 5, max(4, args.steps // 5)
-    ov, se, ov_g, se_g, gc, ga, ca = [], [], [], [], [], [], []
-    n_all = w.M * w.N
-    for _ in range(rounds):
-        us, gm, _, _ = timed_steps(torch, w, plan, dp, b, s1, s2, per, 2)
-        ov.append(us)
-        ov_g.append(gm)
-        us, gm, _, _ = timed_steps(torch, w, plan, dp, b, s1, s1, per, 2)
-        se.append(us)
-        se_g.append(gm)
-        # GEMM + consume of the overlapped run, the GEMM alone and the
-        # consumer alone (whole buffer, full grid), in the same round
-        gc.append(float(np.median(gemm_comm_times(torch, w, plan, dp, b, s1, s2, per))))
-        ga.append(time_gemm(torch, base_plan, dp_base, b, s1, per, 1))
-        ca.append(with_grid((256, 256), lambda: time_loop(
-            torch, lambda: fo.consume_group(b.C, b.peer, b.dst, n_all, w.dtype, None, 0, None, s1), per, 1, s1)))
-    ov_us, serial_us = float(np.median(ov)), float(np.median(se))
-    gc_us, ga_us, ca_us = float(np.median(gc)), float(np.median(ga)), float(np.median(ca))
+    per = max(4, args.steps // 5)
+    rounds = overlap_rounds(torch, w, plan, dp, base_plan, dp_base, b, s1, s2, 5, per)
 
-    # the timed region: exactly `steps` overlapped steps after `warmup` ones
+    # ---- the timed region: exactly `steps` overlapped steps after `warmup` --
     log(f"timed steps: warmup {args.warmup}, steps {args.steps}")
     step_us, gemm_mean_us, gemm_med_us, wall = timed_steps(torch, w, plan, dp, b, s1, s2, args.steps,
                                                            args.warmup)
-
-    # ---- Algorithm 1's estimate vs measurement, every partition ------------
-    pred = predictor_accuracy(torch, w, inp, b, base_plan, dp_base, num_cus, T, flops, s1, s2, args) \
-        if 1 < T <= 8 else None
-
-    # ---- group-size sweep (waves per group) ---------------------------------
-    sweep = {}
-    for g in (w.sweep or ()):
-        if g > T:
-            continue
-        sizes = [g] * (T // g) + ([T % g] if T % g else [])
-        p = make_plan(w, inp, num_cus, sizes=sizes)
-        d = dev_plan(torch, p)
-        torch.cuda.synchronize()
-        us, gm, _, _ = timed_steps(torch, w, p, d, b, s1, s2, max(10, args.steps // 2), 3)
-        sweep[str(g)] = {"groups": sizes, "step_us": round(us, 2), "gemm_us": round(gm, 2)}
-
-    # ---- producer / consumer publication schemes (fo_sync_mode) ------------
-    sync_variants = {}
-    default_modes = fo.get_sync_mode()
-    for pm, cm in ((0, 0), (1, 1), (2, 2)):
-        fo.set_sync_mode(pm, cm)
-        sg = time_gemm(torch, base_plan, dp_base, b, s1, 50, 5)
-        us, gm, _, _ = timed_steps(torch, w, plan, dp, b, s1, s2, max(10, args.steps // 2), 3)
-        sync_variants[f"{pm}{cm}"] = {"signaled_alone_us": round(sg, 2), "overlapped_step_us": round(us, 2),
-                                      "overlapped_gemm_us": round(gm, 2)}
-    fo.set_sync_mode(*default_modes)
-
-    # ---- grid of the consumers beside the GEMM (fo_set_consumer_grid) ------
-    grid_variants = {}
-    default_grid = fo.get_consumer_grid()
-    for nb, nt in ((256, 64), (256, 128), (256, 256), (128, 64), (64, 256), (32, 256)):
-        fo.set_consumer_grid(nb, nt)
-        us, gm, _, _ = timed_steps(torch, w, plan, dp, b, s1, s2, max(10, args.steps // 2), 3)
-        grid_variants[f"{nb}x{nt}"] = {"overlapped_step_us": round(us, 2), "overlapped_gemm_us": round(gm, 2)}
-    fo.set_consumer_grid(*default_grid)
-
-    # ---- a slower interconnect: every consumer launch capped ---------------
-    slow_link = slow_link_report(torch, w, inp, b, num_cus, sig_us, s1, s2) if plan.P > 0 else None
 
     # ---- consistency at full size: overlapped vs serialized output bits ----
     # (every buffer the step writes is poisoned first; 0xFFFF is a NaN)
@@ -674,22 +870,40 @@ def main():
     ref_C, ref_dst, ref_out = b.C.clone(), b.dst.clone(), b.out.clone()
     for buf in (b.C, b.dst, b.out):
         buf.fill_(-1)
-    b.status.zero_()
     run_step(torch, w, plan, dp, b, s1, s2)
     torch.cuda.synchronize()
+    check_status(b, "the consistency runs")
     consistent = bool(torch.equal(ref_out, b.out) and torch.equal(ref_dst, b.dst) and torch.equal(ref_C, b.C))
     if not consistent:
-        raise RuntimeError(
-            "overlapped and serialized runs disagree: C' %d, dst %d, out %d differing elements, status %d" % (
-                int((ref_C != b.C).sum()), int((ref_dst != b.dst).sum()), int((ref_out != b.out).sum()),
-                int(b.status.cpu()[0])))
+        raise RuntimeError("overlapped and serialized runs disagree: C' %d, dst %d, out %d differing elements" % (
+            int((ref_C != b.C).sum()), int((ref_dst != b.dst).sum()), int((ref_out != b.out).sum())))
+    del ref_C, ref_dst, ref_out
 
-    # ---- post-reorder vs the same kernel on an identity map (Table 5 analogue)
+    # ---- post-reorder vs the same kernel on an identity map -----------------
     post_us = time_loop(torch, lambda: fo.post_reorder(plan, dp, b.dst, b.out, b.bias, b.gamma, w.eps,
                                                        w.rmsnorm, s1), 50, 5, s1)
     post_id_us = time_loop(torch, lambda: fo.post_reorder(plan_rm, None, b.C, b.out, b.bias, b.gamma, w.eps,
                                                           w.rmsnorm, s1), 50, 5, s1)
-    post_bytes = 4.0 * w.M * w.N + (4.0 * w.N if (w.bias or w.gamma) else 0.0)
+    post_bytes = 4.0 * w.M * w.N + (2.0 * w.N * (int(w.bias) + int(w.gamma)))
+
+    # ---- Algorithm 1's estimate vs measurement, every partition ------------
+    pred = predictor_accuracy(torch, w, inp, b, base_plan, dp_base, num_cus, T, flops, s1, s2, args) \
+        if 1 < T <= 8 else None
+
+    # ---- Table 5 analogue, group-size sweep ---------------------------------
+    log("Table 5 analogue")
+    t5 = table5(torch, w, inp, b, num_cus, T, s1)
+    log("group-size sweep")
+    sw = sweep(torch, w, inp, num_cus, b, s1, s2, max(10, args.steps // 2))
+
+    # ---- every other workload -------------------------------------------------
+    others = {}
+    if not args.skip_workloads and w.name == HEADLINE:
+        del b
+        torch.cuda.empty_cache()
+        for name in OTHER_WORKLOADS:
+            others[name] = workload_summary(torch, name, num_cus, args.steps)
+            torch.cuda.empty_cache()
 
     # ---- CPU baseline ----------------------------------------------------
     cpu = None
@@ -697,16 +911,28 @@ def main():
         log("CPU oracle baseline")
         cpu = cpu_baseline(w, inp, args.cpu_seconds, plan.sizes, num_cus)
 
-    plain_us, cons_all_us = res["plain_us"], res["cons_all_us"]
     gemm_tflops = flops / gemm_mean_us / 1e6
     value = flops / step_us / 1e6
-    last_share = plan.targets[-1] / tiles if plan.P else 1.0
-    bound_us = max(sig_us + cons_all_us * last_share,
-                   sig_us / T * plan.sizes[0] + cons_all_us) if plan.P else sig_us
+    bound_us = theoretical(plan, rounds["gemm_alone_us"], rounds["consume_alone_us"], post_us)
+    ov = overlap_fields(rounds, bound_us)
+    ov.update({"timed_steps_us": round(step_us, 2), "rounds": 5, "steps_per_round": per,
+               "overlapped_rounds_us": [round(x, 1) for x in rounds["overlapped_rounds_us"]],
+               "serial_rounds_us": [round(x, 1) for x in rounds["serial_rounds_us"]],
+               "predicted_us": round(plan.predicted_us, 2),
+               "paper_context": "up to 1.65x overlap speedup on 4x RTX 4090 over PCIe (multi-GPU collectives; "
+                                "not comparable to this 1-GPU stand-in)"})
+    headline = {"gemm_alone_us": round(sig_us, 2), "gemm_tflops": round(flops / sig_us / 1e6, 2),
+                "gemm_frac_peak": round(flops / sig_us / 1e6 / PEAK_TFLOPS, 4),
+                "gemm_in_step_tflops": round(gemm_tflops, 2),
+                "consumer_GBps": round(cons_bytes_per_elem * n_all / cons_all_us / 1e3, 1),
+                "post_reorder_GBps": round(post_bytes / post_us / 1e3, 1), "step_tflops": round(value, 2),
+                "overlap": {k: ov[k] for k in ("speedup_vs_serial", "overlapped_gemm_consume_over_max",
+                                               "fraction_of_theoretical_speedup")}}
     line = {
         "metric": METRIC,
         "value": round(value, 2),
         "unit": "TFLOP/s",
+        "value_is": "GEMM flops / time of the whole overlapped step (GEMM, consumers, post-reorder)",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -722,41 +948,33 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": round(PEAK_TFLOPS, 1),
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_TFLOPS, 4),
                      "traffic": traffic_bytes(w)},
-        "gemm": {"signaled_overlapped_us": round(gemm_mean_us, 2), "signaled_overlapped_median_us": round(gemm_med_us, 2),
-                 "signaled_alone_us": round(sig_us, 2), "plain_alone_us": round(plain_us, 2),
-                 "plain_tflops": round(flops / plain_us / 1e6, 2),
+        "gemm": {"signaled_overlapped_us": round(gemm_mean_us, 2),
+                 "signaled_overlapped_median_us": round(gemm_med_us, 2),
+                 "signaled_alone_us": round(sig_us, 2),
+                 "plain_signalled_alone_us": round(plain_sig_us, 2),
+                 "plain_static_alone_us": round(plain_static_us, 2),
                  "signaled_tflops": round(flops / sig_us / 1e6, 2),
-                 "interference_pct": round((sig_us / plain_us - 1) * 100, 2),
+                 "plain_signalled_tflops": round(flops / plain_sig_us / 1e6, 2),
+                 "plain_static_tflops": round(flops / plain_static_us / 1e6, 2),
+                 "interference_pct": round((sig_us / plain_sig_us - 1) * 100, 2),
+                 "interference_vs_static_pct": round((sig_us / plain_static_us - 1) * 100, 2),
                  "pct_peak_signaled": round(flops / sig_us / 1e6 / PEAK_TFLOPS * 100, 2)},
-        "consumer": {"whole_buffer_us": round(cons_all_us, 2), "GBps": round(res["cons_gbs"], 1),
-                     "frac_hbm": round(res["cons_gbs"] / PEAK_HBM_GBS, 4),
-                     "whole_buffer_beside_gemm_grid_us": round(res["cons_gentle_us"], 2),
-                     "beside_gemm_grid": "%dx%d" % default_grid},
+        "consumer": {"whole_buffer_us": round(cons_all_us, 2),
+                     "GBps": round(cons_bytes_per_elem * n_all / cons_all_us / 1e3, 1),
+                     "frac_hbm": round(cons_bytes_per_elem * n_all / cons_all_us / 1e3 / PEAK_HBM_GBS, 4),
+                     "whole_buffer_beside_gemm_grid_us": round(ys[-1], 2),
+                     "beside_gemm_grid": "%dx%d" % fo.get_consumer_grid()},
         "post_reorder": {"us": round(post_us, 2), "identity_map_us": round(post_id_us, 2),
                          "GBps": round(post_bytes / post_us / 1e3, 1),
+                         "frac_hbm": round(post_bytes / post_us / 1e3 / PEAK_HBM_GBS, 4),
                          "overhead_pct": round((post_us / post_id_us - 1) * 100, 2)},
-        "overlap": {"timed_steps_us": round(step_us, 2),
-                    "overlapped_step_us": round(ov_us, 2), "serial_step_us": round(serial_us, 2),
-                    "rounds": rounds, "steps_per_round": per,
-                    "overlapped_rounds_us": [round(x, 1) for x in ov],
-                    "serial_rounds_us": [round(x, 1) for x in se],
-                    "gemm_in_overlapped_us": round(float(np.median(ov_g)), 2),
-                    "gemm_in_serial_us": round(float(np.median(se_g)), 2),
-                    "speedup_vs_serial": round(serial_us / ov_us, 4),
-                    "gemm_consume_overlapped_us": round(gc_us, 2),
-                    "gemm_alone_us": round(ga_us, 2), "consume_alone_us": round(ca_us, 2),
-                    "overlapped_gemm_consume_over_max": round(gc_us / max(ga_us, ca_us), 4),
-                    "theoretical_bound_us": round(bound_us + post_us, 2),
-                    "predicted_us": round(plan.predicted_us, 2),
-                    "paper_context": "up to 1.65x overlap speedup on 4x RTX 4090 over PCIe (multi-GPU "
-                                     "collectives; not comparable to this 1-GPU stand-in)"},
-        "sweep_waves_per_group": sweep,
+        "overlap": ov,
+        "overlapped_equals_serial_bits": consistent,
+        "table5": t5,
+        "sweep_waves_per_group": sw,
         "predictor": None if pred is None else {k: v for k, v in pred.items() if k != "phase"},
         "planner": planner,
-        "sync_modes": {"default": list(default_modes), "variants": sync_variants,
-                       "overlapped_equals_serial_bits": consistent},
-        "consumer_grid": {"default": "%dx%d" % default_grid, "variants": grid_variants},
-        "slow_link": slow_link,
+        "workloads": dict({w.name: headline}, **others),
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
     }

@@ -239,6 +239,45 @@ size_t fo_plan_device_bytes(const fo_plan* plan);
 fo_status fo_plan_to_device(const fo_plan* plan, void* dev_buf, size_t bytes, void* stream);
 
 /*
+ * Per-call options of the GPU entry points (fo_gemm_signal_reorder,
+ * fo_consume_group, fo_run_overlapped). Every such call takes a
+ * `const fo_options*`; NULL means the process defaults. fo_options_init
+ * fills *o with those defaults as they stand at the time of the call (the
+ * fo_set_* calls below and their environment variables), so that a caller
+ * changes only what it needs and two layers can run with different options
+ * in one process. The library reads the struct during the call only.
+ */
+typedef struct {
+    int32_t sync_producer;    /* fo_sync_mode of the GEMM epilogue             */
+    int32_t sync_consumer;    /* fo_sync_mode of the consumer launches         */
+    int32_t consumer_blocks;  /* grid cap of consumers beside the GEMM, 1..256 */
+    int32_t consumer_threads; /* their workgroup size: 64, 128 or 256          */
+    int64_t poll_timeout_us;  /* bound of every device-side wait, > 0          */
+    /* Benchmark and diagnostic controls; the path itself never needs them. */
+    int32_t consumer_limit;   /* cap on the workgroups of EVERY consumer launch
+                                 (1..256), 0 = none: a stand-in for a slower
+                                 interconnect (the consumer's bandwidth grows
+                                 with its workgroups); under a cap every launch
+                                 uses the variant that fits beside the GEMM   */
+    int32_t reserved0;        /* must be 0                                     */
+    uint64_t* tile_trace;     /* tile timeline (device memory, 8-byte aligned),
+                                 NULL = none: each GEMM launch writes, for every
+                                 dispatch position p < tile_trace_capacity, four
+                                 uint64 at tile_trace[4p]: the device wall clock
+                                 (fo_device_wall_clock_khz) when the tile
+                                 started and when all of its stores had
+                                 completed, the chiplet (XCC_ID register, high
+                                 32 bits) and hardware id (HW_ID, low 32 bits)
+                                 of its compute unit, and the workgroup index.
+                                 Tracing adds a store drain and a barrier per
+                                 tile (the timeline of Section 2.1.1, Fig. 3) */
+    int64_t tile_trace_capacity; /* >= 1 when tile_trace is set               */
+} fo_options;
+
+/* Process defaults into *o. FO_ERR_ARG if o is NULL. */
+fo_status fo_options_init(fo_options* o);
+
+/*
  * fo_gemm_signal_reorder -- C = A x B with the reordering, signalling
  * epilogue (Section 3.2 Approach; Section 3.3 Approach; Section 5: the
  * reorder sits in the epilogue, the main loop is untouched).
@@ -258,13 +297,17 @@ fo_status fo_plan_to_device(const fo_plan* plan, void* dev_buf, size_t bytes, vo
  *             pool_base[s*B+b] + (rank of row r among rows of tile row tm
  *             bound for b), b = row_bucket[tm*tile_m + r].
  * counters: at least P + FO_DISPENSER_WORDS uint32 (fo_plan_num_counters
- * also counts the words fo_run_overlapped needs), zeroed by the caller before
- * the launch and before any consumer of this run starts (see
- * fo_reset_counters); NULL = no signalling. When a tile's stores
- * are complete, one workgroup-level agent-scope release increment is made on
- * counters[group of its slot]; when the GEMM is done, counters[j] ==
- * target_j for every j < P. counters[P ..] hand out tile positions to the
- * GEMM's workgroups (their final values are unspecified).
+ * also counts the words fo_run_overlapped needs); NULL = no signalling.
+ * counters[0, P) are the group counters: zeroed by the caller before the
+ * launch and before any consumer of this run starts (see fo_reset_counters).
+ * When a tile's stores are complete and visible to every chiplet, one
+ * agent-scope increment is made on counters[group of its slot]; when the
+ * GEMM is done, counters[j] == target_j for every j < P.
+ * counters[P, P + FO_DISPENSER_WORDS) hand out tile positions to the GEMM's
+ * workgroups: they must be zero before the first launch on the array, and
+ * every launch that runs to its end leaves them zero again (the last
+ * workgroup to find its position class exhausted clears the class's word),
+ * so back-to-back launches need not clear them.
  * The GEMM runs min(tiles, W) persistent workgroups (W = the plan's wave
  * width). With counters, each takes its next dispatch position from an
  * atomic counter when it finishes a tile, so positions start in increasing
@@ -277,7 +320,8 @@ fo_status fo_plan_to_device(const fo_plan* plan, void* dev_buf, size_t bytes, vo
  */
 fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan,
                                  const void* A, const void* W, void* C_out,
-                                 uint32_t* counters, void* stream);
+                                 uint32_t* counters, void* stream,
+                                 const fo_options* options);
 
 /*
  * fo_consume_group -- the communication stand-in for one contiguous segment
@@ -292,15 +336,18 @@ fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan,
  *                  of this GPU's partial with one peer partial)
  *   peer == NULL:  dst[i] = src[i]                  (All-to-All copy)
  * counter == NULL: no wait (one launch). The wait is bounded
- * (fo_set_poll_timeout_us); on timeout the segment is not written and
- * *status_word (if non-NULL, device uint32, caller-zeroed) gets bit 0 set.
+ * (options->poll_timeout_us); on timeout the segment is not written and
+ * *status_word (if non-NULL, device uint32) gets bit 0 set; the library
+ * never clears it. The launch uses options->consumer_blocks and
+ * consumer_threads (capped by consumer_limit) and the consumer sync mode.
  * Buffers must not overlap. Any alignment works; 16-byte-aligned pointers
  * take the vector path.
- * Errors: FO_ERR_ARG (null src/dst with len > 0, len < 0, bad dtype).
+ * Errors: FO_ERR_ARG (null src/dst with len > 0, len < 0, bad dtype, an
+ * option out of range).
  */
 fo_status fo_consume_group(const void* src, const void* peer, void* dst, int64_t len,
                            int32_t dtype, const uint32_t* counter, uint32_t target,
-                           uint32_t* status_word, void* stream);
+                           uint32_t* status_word, void* stream, const fo_options* options);
 
 /*
  * fo_post_reorder -- post-communication reorder fused into the following
@@ -334,21 +381,30 @@ fo_status fo_reset_counters(uint32_t* counters, int32_t n, void* stream);
  *                -> fo_post_reorder (if out != NULL)
  *   comm_stream: gate kernel -> one consumer launch per group
  * The two streams hand work to each other on the device, not with events:
- * the reset kernel zeroes the status word and counters[0, P +
- * FO_DISPENSER_WORDS + 2) except the gate word counters[P +
- * FO_DISPENSER_WORDS], then writes a tag unique to the run into the gate
- * word, and the gate kernel (one wave) holds the consumers until it reads
- * that tag; the final consumer launch adds its finished workgroups into
- * counters[P + FO_DISPENSER_WORDS + 1], and the done wait (one wave) holds
- * the post-reorder until all have. Both waits are bounded like a consumer's
- * (fo_set_poll_timeout_us): on timeout bit 0 of the status word is set and
- * the run's dst and out are unspecified.
+ * the reset kernel zeroes counters[0, P + FO_DISPENSER_WORDS), writes the
+ * run's tag (a process-wide sequence number) into the done word
+ * counters[P + FO_DISPENSER_WORDS + 1] with a count of zero, then writes the
+ * tag into the gate word counters[P + FO_DISPENSER_WORDS]; the gate kernel
+ * (one wave) holds the consumers until it reads that tag; each workgroup of
+ * the final consumer launch adds 1 to the done word only while the word
+ * carries its own run's tag, and the done wait (one wave) holds the
+ * post-reorder until the count reaches the launch's grid. A consumer of an
+ * earlier run that finishes late therefore does not count for a later run
+ * (it can only race with the later run's reset, the check and the add being
+ * two steps, if a wait of the earlier run timed out: then the status bit is
+ * already set).
+ * Both waits are bounded like a consumer's (options->poll_timeout_us): on
+ * timeout bit 0 of the status word is set and the run's dst and out are
+ * unspecified. The status word is sticky: the library only sets bits, the
+ * caller clears it, so a timeout of one run stays visible after later runs
+ * queued behind it. A gate that gives up because a later run's tag has
+ * already arrived leaves the word as it is (that run is not delayed).
  * A group's consumer is one wait kernel on the group's counter and one
  * streaming kernel that does what fo_consume_group does for each of the
  * group's plan segments (fo_plan_segments: 1, R or B of them). Every group
  * but the last uses the grid of fo_get_consumer_grid(); the last group,
  * which runs after the GEMM, uses up to 256 workgroups of 256 threads (as do
- * all groups of a serialized run); fo_set_consumer_limit caps them all.
+ * all groups of a serialized run); options->consumer_limit caps them all.
  * With comm_stream == gemm_stream (or NULL) the same work runs serialized
  * on gemm_stream, without the handoffs and without signalling. A plan of one
  * group has nothing to overlap (its consumer can only start after the whole
@@ -367,8 +423,10 @@ fo_status fo_reset_counters(uint32_t* counters, int32_t n, void* stream);
  * gemm_begin_event / gemm_end_event: optional caller-owned hipEvent_t (as
  * void*) recorded on gemm_stream right before and after the GEMM launch, so
  * a caller can time the GEMM inside the overlapped run; NULL = none.
+ * options: as for the three calls the run makes (NULL = process defaults).
  * Errors: FO_ERR_ARG (no plan or dst; overlapped without counters or with a
- * null gemm_stream), and those of the three calls the run makes.
+ * null gemm_stream; an option out of range), and those of the three calls
+ * the run makes.
  */
 fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan,
                             const void* A, const void* W, void* C_out,
@@ -376,7 +434,8 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan,
                             const void* bias, const void* gamma, float eps,
                             int32_t do_rmsnorm, uint32_t* counters,
                             uint32_t* status_word, void* gemm_stream, void* comm_stream,
-                            void* gemm_begin_event, void* gemm_end_event);
+                            void* gemm_begin_event, void* gemm_end_event,
+                            const fo_options* options);
 
 /*
  * How the producer (GEMM epilogue) publishes a finished tile and how the
@@ -394,7 +453,8 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan,
  *     write-back); consumer: the group is read with device-coherent loads
  *     after the counter is seen (no invalidation).
  * Default: FO_SYNC_COHERENT for both; env FO_SYNC_PRODUCER / FO_SYNC_CONSUMER
- * (0, 1, 2) override at load time. Process-wide.
+ * (0, 1, 2) override at load time. Process default of fo_options.sync_producer
+ * and sync_consumer (fo_options_init).
  */
 typedef enum { FO_SYNC_FENCE_ALL = 0, FO_SYNC_FENCE_ONE = 1, FO_SYNC_COHERENT = 2 } fo_sync_mode;
 fo_status fo_set_sync_mode(int32_t producer, int32_t consumer);
@@ -406,37 +466,17 @@ void fo_get_sync_mode(int32_t* producer, int32_t* consumer);
  * 256); default 256 x 256. A smaller grid streams a group more slowly and
  * spreads its memory traffic over more of the GEMM's run. Env
  * FO_CONSUMER_BLOCKS / FO_CONSUMER_THREADS override at load time.
- * Process-wide; FO_ERR_ARG outside the ranges. */
+ * Process default of fo_options.consumer_blocks / consumer_threads;
+ * FO_ERR_ARG outside the ranges. */
 fo_status fo_set_consumer_grid(int32_t max_blocks, int32_t threads);
 void fo_get_consumer_grid(int32_t* max_blocks, int32_t* threads);
 
-/* Cap on the workgroups of every consumer launch -- all groups of overlapped
- * and serialized runs (the last group included) and fo_consume_group -- at
- * max_blocks (1 .. 256); 0 = no cap (the default). A stand-in for a slower
- * interconnect in benchmarks: the consumer's bandwidth grows with its
- * workgroups, so a cap slows the communication side of a run without
- * changing what it computes. Under a cap every launch uses the consumer
- * variant that fits beside the GEMM, so that the emulated link streams at one
- * speed in overlapped and serialized runs. Process-wide; FO_ERR_ARG outside
- * the range. */
-fo_status fo_set_consumer_limit(int32_t max_blocks);
-int32_t fo_get_consumer_limit(void);
-
-/* Upper bound of one consumer wait, in microseconds (default 2 s; env
- * FO_POLL_TIMEOUT_US overrides at load time). */
+/* Upper bound of one device-side wait, in microseconds (default 2 s; env
+ * FO_POLL_TIMEOUT_US overrides at load time): the process default of
+ * fo_options.poll_timeout_us. */
 void fo_set_poll_timeout_us(int64_t us);
 int64_t fo_get_poll_timeout_us(void);
 
-/* Tile timeline (the wave pattern of Section 2.1.1, Figure 3). While set,
- * every fo_gemm_signal_reorder launch writes, for each dispatch position
- * p < capacity_tiles, four uint64 at trace[4p]: the device wall clock
- * (s_memrealtime ticks, fo_device_wall_clock_khz) when the tile started, the
- * wall clock when all of its stores had completed, the chiplet (XCC_ID
- * register, high 32 bits) and hardware id (HW_ID register, low 32 bits) of
- * the compute unit that ran it, and the workgroup index. Tracing adds a
- * store drain and a barrier per tile. trace: caller-owned device memory,
- * 8-byte aligned; NULL stops tracing. Process-wide. */
-fo_status fo_set_tile_trace(uint64_t* trace, int64_t capacity_tiles);
 /* Ticks per millisecond of the device wall clock of the current device. */
 fo_status fo_device_wall_clock_khz(int32_t* khz);
 

@@ -21,7 +21,7 @@ __all__ = [
     "FoError", "Plan", "PlanCache", "plan_groups", "gemm_signal_reorder", "consume_group",
     "post_reorder", "reset_counters", "run_overlapped", "set_poll_timeout_us",
     "get_poll_timeout_us", "device_num_cus", "set_sync_mode", "get_sync_mode",
-    "set_consumer_grid", "get_consumer_grid", "set_consumer_limit", "get_consumer_limit", "set_tile_trace", "device_wall_clock_khz", "LIB_PATH",
+    "set_consumer_grid", "get_consumer_grid", "Options", "options", "device_wall_clock_khz", "LIB_PATH",
     "FP16", "BF16", "TILE", "SUBTILE", "SUBTOKEN", "ROWMAJOR",
 ]
 
@@ -67,6 +67,16 @@ class _Grouping(ctypes.Structure):
                 ("all_dest_bytes", ctypes.c_int32)]
 
 
+class _Options(ctypes.Structure):
+    _fields_ = [("sync_producer", ctypes.c_int32), ("sync_consumer", ctypes.c_int32),
+                ("consumer_blocks", ctypes.c_int32), ("consumer_threads", ctypes.c_int32),
+                ("poll_timeout_us", ctypes.c_int64), ("consumer_limit", ctypes.c_int32),
+                ("reserved0", ctypes.c_int32), ("tile_trace", ctypes.c_void_p),
+                ("tile_trace_capacity", ctypes.c_int64)]
+
+
+Options = _Options
+
 _lib = None
 
 
@@ -102,20 +112,19 @@ def lib() -> ctypes.CDLL:
     L.fo_plan_predicted_us.argtypes, L.fo_plan_predicted_us.restype = [vp], ctypes.c_double
     L.fo_plan_device_bytes.argtypes, L.fo_plan_device_bytes.restype = [vp], ctypes.c_size_t
     L.fo_plan_to_device.argtypes = [vp, vp, ctypes.c_size_t, vp]
-    L.fo_gemm_signal_reorder.argtypes = [vp, vp, vp, vp, vp, vp, vp]
-    L.fo_consume_group.argtypes = [vp, vp, vp, i64, i32, vp, u32, vp, vp]
+    po = ctypes.POINTER(_Options)
+    L.fo_options_init.argtypes, L.fo_options_init.restype = [po], ctypes.c_int
+    L.fo_gemm_signal_reorder.argtypes = [vp, vp, vp, vp, vp, vp, vp, po]
+    L.fo_consume_group.argtypes = [vp, vp, vp, i64, i32, vp, u32, vp, vp, po]
     L.fo_post_reorder.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_float, i32, vp]
     L.fo_reset_counters.argtypes = [vp, i32, vp]
     L.fo_run_overlapped.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, i32,
-                                    vp, vp, vp, vp, vp, vp]
+                                    vp, vp, vp, vp, vp, vp, po]
     L.fo_set_sync_mode.argtypes, L.fo_set_sync_mode.restype = [i32, i32], ctypes.c_int
     L.fo_get_sync_mode.argtypes = [pi32, pi32]
     L.fo_set_consumer_grid.argtypes, L.fo_set_consumer_grid.restype = [i32, i32], ctypes.c_int
-    L.fo_set_tile_trace.argtypes, L.fo_set_tile_trace.restype = [vp, i64], ctypes.c_int
     L.fo_device_wall_clock_khz.argtypes, L.fo_device_wall_clock_khz.restype = [pi32], ctypes.c_int
     L.fo_get_consumer_grid.argtypes = [pi32, pi32]
-    L.fo_set_consumer_limit.argtypes, L.fo_set_consumer_limit.restype = [i32], ctypes.c_int
-    L.fo_get_consumer_limit.restype = i32
     L.fo_set_poll_timeout_us.argtypes = [i64]
     L.fo_get_poll_timeout_us.restype = i64
     L.fo_device_num_cus.argtypes = [i32, pi32]
@@ -384,22 +393,47 @@ class PlanCache:
         return res
 
 
-def gemm_signal_reorder(plan: Plan, dev_plan, A, W, C_out, counters=None, stream=None) -> None:
+def options(**fields) -> _Options:
+    """fo_options: the process defaults (fo_options_init) with the given
+    fields changed (sync_producer, sync_consumer, consumer_blocks,
+    consumer_threads, poll_timeout_us, consumer_limit, tile_trace: a device
+    buffer, tile_trace_capacity)."""
+    o = _Options()
+    _check(lib().fo_options_init(ctypes.byref(o)))
+    for k, v in fields.items():
+        if k not in dict(_Options._fields_):
+            raise TypeError(f"unknown option {k!r}")
+        setattr(o, k, _ptr(v) if k == "tile_trace" else int(v))
+    return o
+
+
+def _opts(o):
+    """A pointer to an fo_options (None = the process defaults); a dict of
+    fields is turned into options(**dict)."""
+    if o is None:
+        return None
+    if isinstance(o, dict):
+        o = options(**o)
+    return ctypes.byref(o)
+
+
+def gemm_signal_reorder(plan: Plan, dev_plan, A, W, C_out, counters=None, stream=None, opts=None) -> None:
     _need(A, 2 * plan.M * plan.K, "A")
     _need(W, 2 * plan.N * plan.K, "W")
     _need(C_out, 2 * plan.M * plan.N, "C_out")
     _need(counters, 4 * (plan.P + DISPENSER_WORDS), "counters")
     _check(lib().fo_gemm_signal_reorder(plan.handle, _ptr(dev_plan), _ptr(A), _ptr(W), _ptr(C_out),
-                                        _ptr(counters), _stream(stream)))
+                                        _ptr(counters), _stream(stream), _opts(opts)))
 
 
 def consume_group(src, peer, dst, length: int, dtype, counter=None, target: int = 0,
-                  status_word=None, stream=None) -> None:
+                  status_word=None, stream=None, opts=None) -> None:
     _need(src, 2 * int(length), "src")
     _need(peer, 2 * int(length), "peer")
     _need(dst, 2 * int(length), "dst")
     _check(lib().fo_consume_group(_ptr(src), _ptr(peer), _ptr(dst), int(length), _DTYPES[dtype],
-                                  _ptr(counter), int(target), _ptr(status_word), _stream(stream)))
+                                  _ptr(counter), int(target), _ptr(status_word), _stream(stream),
+                                  _opts(opts)))
 
 
 def post_reorder(plan: Plan, dev_plan, src, out, bias=None, gamma=None, eps: float = 1e-6,
@@ -419,7 +453,7 @@ def reset_counters(counters, n: int, stream=None) -> None:
 def run_overlapped(plan: Plan, dev_plan, A, W, C_out, peer, dst, out=None, bias=None, gamma=None,
                    eps: float = 1e-6, do_rmsnorm: bool = False, counters=None, status_word=None,
                    gemm_stream=None, comm_stream=None, gemm_begin_event=None,
-                   gemm_end_event=None) -> None:
+                   gemm_end_event=None, opts=None) -> None:
     _need(A, 2 * plan.M * plan.K, "A")
     _need(W, 2 * plan.N * plan.K, "W")
     _need(C_out, 2 * plan.M * plan.N, "C_out")
@@ -434,7 +468,7 @@ def run_overlapped(plan: Plan, dev_plan, A, W, C_out, peer, dst, out=None, bias=
                                    _ptr(peer), _ptr(dst), _ptr(out), _ptr(bias), _ptr(gamma),
                                    float(eps), int(bool(do_rmsnorm)), _ptr(counters),
                                    _ptr(status_word), _stream(gemm_stream), _stream(comm_stream),
-                                   _event(gemm_begin_event), _event(gemm_end_event)))
+                                   _event(gemm_begin_event), _event(gemm_end_event), _opts(opts)))
 
 
 SYNC_FENCE_ALL, SYNC_FENCE_ONE, SYNC_COHERENT = 0, 1, 2
@@ -461,22 +495,6 @@ def get_consumer_grid():
     b, t = ctypes.c_int32(), ctypes.c_int32()
     lib().fo_get_consumer_grid(ctypes.byref(b), ctypes.byref(t))
     return int(b.value), int(t.value)
-
-
-def set_consumer_limit(max_blocks: int) -> None:
-    """Cap every consumer launch at `max_blocks` workgroups (0 = no cap): a
-    stand-in for a slower interconnect in benchmarks."""
-    _check(lib().fo_set_consumer_limit(int(max_blocks)))
-
-
-def get_consumer_limit() -> int:
-    return int(lib().fo_get_consumer_limit())
-
-
-def set_tile_trace(trace, capacity_tiles: int = 0) -> None:
-    """Record the tile timeline of subsequent GEMM launches into `trace`
-    (device buffer of 4 x uint64 per tile); None stops tracing."""
-    _check(lib().fo_set_tile_trace(_ptr(trace), int(capacity_tiles) if trace is not None else 0))
 
 
 def device_wall_clock_khz() -> int:

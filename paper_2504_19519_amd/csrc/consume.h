@@ -25,7 +25,9 @@ struct ConsumeArgs {
     uint32_t target;
     uint32_t* status;            // bit 0 set on a timed-out wait (may be nullptr)
     uint64_t timeout_ticks;      // wall-clock ticks
-    uint32_t* done;              // non-null: each workgroup adds 1 when its stores are visible
+    uint32_t* done;              // non-null: each workgroup adds 1 when its stores are visible,
+                                 // while the word's high half equals done_tag's
+    uint32_t done_tag;           // run tag of the done word (done_tag_of)
     int32_t nseg;                // 1 .. kMaxConsumeSegments
     ConsumeSegment seg[kMaxConsumeSegments];
 };
@@ -45,12 +47,19 @@ hipError_t launch_wait(const uint32_t* counter, uint32_t target, uint32_t* statu
                        hipStream_t s);
 
 // Tags of the start handoff of an overlapped run: the run's reset kernel
-// writes its tag into the gate word once the counters are zero; the gate
-// kernel on the other stream waits for that tag. A gate that times out
-// replaces the word's old value by tag | kGateTimedOut, which the reset
-// kernel, if it runs later, turns into bit 0 of the status word.
+// writes its tag (bit 31 and 30 bits of the run's sequence number) into the
+// gate word once the counters are zero; the gate kernel on the other stream
+// waits for that tag. A gate that times out while the word holds an older
+// run's tag replaces it by tag | kGateTimedOut, which the reset kernel, if it
+// runs later, turns into bit 0 of the status word; a gate that times out
+// after a later run's tag has arrived only raises the status bit.
 constexpr uint32_t kGateTag = 0x80000000u;
 constexpr uint32_t kGateTimedOut = 0x40000000u;
+constexpr uint32_t kGateSeqMask = kGateTimedOut - 1;
+// Done word of an overlapped run: the low 16 bits of the run's sequence
+// number in the high half, the count of finished final-consumer workgroups
+// (at most kMaxConsumeBlocks) in the low half.
+__host__ __device__ inline uint32_t done_tag_of(uint32_t seq) { return (seq & 0xFFFFu) << 16; }
 hipError_t launch_gate(uint32_t* gate, uint32_t tag, uint32_t* status, uint64_t timeout_ticks, hipStream_t s);
 
 }  // namespace fo

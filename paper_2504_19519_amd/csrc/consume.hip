@@ -92,8 +92,9 @@ __global__ __launch_bounds__(64) void wait_kernel(const uint32_t* counter, uint3
 // the run's tag, which the run's reset kernel writes with a release once the
 // counters are zero and the previous run's post-reorder, ordered before it
 // on the GEMM stream, has finished reading the destination buffer. On
-// timeout the lane marks the word (compare-and-swap, so a tag that arrives
-// meanwhile still wins) and raises bit 0 of the status word.
+// timeout the lane raises bit 0 of the status word and, unless the word
+// already holds a later run's tag (which must not be held up), marks the
+// word (compare-and-swap, so a tag that arrives meanwhile still wins).
 __global__ __launch_bounds__(64) void gate_kernel(uint32_t* gate, uint32_t tag, uint32_t* status,
                                                   uint64_t timeout_ticks) {
     if (threadIdx.x != 0) return;
@@ -103,6 +104,13 @@ __global__ __launch_bounds__(64) void gate_kernel(uint32_t* gate, uint32_t tag, 
         __builtin_amdgcn_s_sleep(8);
         v = __hip_atomic_load(gate, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (v != tag && wall_clock64() - t0 > timeout_ticks) {
+            // a later run's tag (sequence ahead of ours, modulo 2^30)
+            const bool later = (v & (kGateTag | kGateTimedOut)) == kGateTag &&
+                               (int32_t)(((v - tag) & kGateSeqMask) << 2) > 0;
+            if (later) {
+                if (status) __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                return;
+            }
             if (__hip_atomic_compare_exchange_strong(gate, &v, tag | kGateTimedOut, __ATOMIC_RELAXED,
                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
                 if (status) __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -328,7 +336,18 @@ __global__ __launch_bounds__(kMaxThreads) void consume_kernel(const ConsumeArgs 
     if constexpr (WT) {
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         __syncthreads();
-        if (threadIdx.x == 0) __hip_atomic_fetch_add(a.done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (threadIdx.x == 0) {
+            // Count only for this launch's own run: once a later run's reset
+            // has put its tag into the word, a late workgroup leaves it alone.
+            // (A plain add after the check: a compare-and-swap loop would
+            // serialise the grid's workgroups on one word, about a
+            // microsecond each. A late workgroup can only race with a later
+            // run's reset if an earlier wait of the stream pair timed out,
+            // which the sticky status bit already reports.)
+            const uint32_t v = __hip_atomic_load(a.done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if ((v & 0xFFFF0000u) == a.done_tag)
+                __hip_atomic_fetch_add(a.done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
 }
 

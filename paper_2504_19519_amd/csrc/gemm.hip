@@ -192,11 +192,21 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
     // position always runs on the chiplet the dispatch order meant it for,
     // and a workgroup that is never scheduled holds no position back);
     // without one, workgroup b takes b, b + grid, b + 2 grid, ...
+    // Every workgroup of a class makes exactly one claim past the class's
+    // positions (its last), so the claims of one launch return 0 .. n_cls +
+    // w_cls - 1; the workgroup that gets the last value is the word's last
+    // user in this launch and leaves it zero for the next launch. A value
+    // past the class's positions (also one left over from elsewhere) ends
+    // the workgroup's loop.
     const int D = a.num_dispensers;
     const int cls = a.dispenser ? (int)(blockIdx.x % (unsigned)D) : 0;
+    const uint32_t n_cls = a.dispenser ? (uint32_t)((tiles - cls + D - 1) / D) : 0u;
+    const uint32_t w_cls = a.dispenser ? (uint32_t)(((int)gridDim.x - cls + D - 1) / D) : 0u;
     auto claim = [&]() -> int {
-        return cls + D * (int)__hip_atomic_fetch_add(a.dispenser + cls, 1u, __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_AGENT);
+        const uint32_t v = __hip_atomic_fetch_add(a.dispenser + cls, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (v == n_cls + w_cls - 1u)
+            __hip_atomic_store(a.dispenser + cls, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return v < n_cls ? cls + D * (int)v : tiles;
     };
     const bool coherent = a.counters && a.sync == FO_SYNC_COHERENT;
     auto signal = [&](int group) {

@@ -54,17 +54,44 @@ std::atomic<int> g_consumer_threads{[] {
     return valid_threads(t) ? t : 256;
 }()};
 
-// Cap on the workgroups of every consumer launch (0 = none): a stand-in for
-// a slower interconnect in benchmarks (fo_set_consumer_limit).
-std::atomic<int> g_consumer_limit{0};
-int limited(int blocks) {
-    const int l = g_consumer_limit.load(std::memory_order_relaxed);
-    return l > 0 && l < blocks ? l : blocks;
+fo_options defaults() {
+    fo_options o{};
+    o.sync_producer = g_sync_producer.load(std::memory_order_relaxed);
+    o.sync_consumer = g_sync_consumer.load(std::memory_order_relaxed);
+    o.consumer_blocks = g_consumer_blocks.load(std::memory_order_relaxed);
+    o.consumer_threads = g_consumer_threads.load(std::memory_order_relaxed);
+    o.poll_timeout_us = poll_timeout_us();
+    return o;
 }
 
-// Tile timeline buffer of the GEMM launches (fo_set_tile_trace).
-std::atomic<uint64_t*> g_trace{nullptr};
-std::atomic<int64_t> g_trace_cap{0};
+// The options of one call: the caller's, checked, or the process defaults.
+fo_status resolve(const fo_options* in, fo_options* out) {
+    if (!in) {
+        *out = defaults();
+        return FO_OK;
+    }
+    const fo_options& o = *in;
+    if (o.sync_producer < FO_SYNC_FENCE_ALL || o.sync_producer > FO_SYNC_COHERENT ||
+        o.sync_consumer < FO_SYNC_FENCE_ALL || o.sync_consumer > FO_SYNC_COHERENT)
+        return fail(FO_ERR_ARG, "options: sync modes are 0, 1 or 2");
+    if (o.consumer_blocks < 1 || o.consumer_blocks > kMaxConsumeBlocks)
+        return fail(FO_ERR_ARG, "options: consumer_blocks must be in [1, 256]");
+    if (!valid_threads(o.consumer_threads)) return fail(FO_ERR_ARG, "options: consumer_threads must be 64, 128 or 256");
+    if (o.poll_timeout_us <= 0) return fail(FO_ERR_ARG, "options: poll_timeout_us must be > 0");
+    if (o.consumer_limit < 0 || o.consumer_limit > kMaxConsumeBlocks)
+        return fail(FO_ERR_ARG, "options: consumer_limit must be 0 (no cap) or in [1, 256]");
+    if (o.reserved0 != 0) return fail(FO_ERR_ARG, "options: reserved0 must be 0");
+    if (o.tile_trace && o.tile_trace_capacity < 1) return fail(FO_ERR_ARG, "options: tile_trace_capacity must be >= 1");
+    if (o.tile_trace && (reinterpret_cast<uintptr_t>(o.tile_trace) & 7))
+        return fail(FO_ERR_ARG, "options: tile_trace must be 8-byte aligned");
+    *out = o;
+    return FO_OK;
+}
+
+// Workgroups of a consumer launch under the options' cap (0 = none).
+int limited(const fo_options& o, int blocks) {
+    return o.consumer_limit > 0 && o.consumer_limit < blocks ? o.consumer_limit : blocks;
+}
 
 constexpr int kMaxDevices = 64;
 std::atomic<int64_t> g_clock_khz[kMaxDevices];   // 0 = unknown
@@ -97,19 +124,18 @@ __global__ void fill_u32_kernel(uint32_t* p, int32_t n, uint32_t v) {
 }
 
 // Start of an overlapped run, one workgroup on the GEMM stream: zero the
-// status word, the group and position counters (n words) and the done word,
-// make the zeros visible device-wide, then exchange the gate word for the
-// run's tag (the start handoff that the gate kernel on the consumer stream
-// waits for). If a gate of this run timed out before, the word holds the
-// tag's timed-out mark: the status word then gets bit 0 back. gate == NULL:
-// only the zeroing (a run without a consumer stream).
+// group and position counters (n words), set the done word to the run's
+// done tag with a count of zero, make both visible device-wide, then
+// exchange the gate word for the run's tag (the start handoff that the gate
+// kernel on the consumer stream waits for). If a gate of this run timed out
+// before, the word holds the tag's timed-out mark: the status word then gets
+// bit 0 (the status word is never cleared here: its bits are sticky).
+// gate == NULL: only the zeroing.
 __global__ __launch_bounds__(256) void reset_run_kernel(uint32_t* counters, int32_t n, uint32_t* done,
-                                                        uint32_t* status, uint32_t* gate, uint32_t tag) {
+                                                        uint32_t done_tag, uint32_t* status, uint32_t* gate,
+                                                        uint32_t tag) {
     for (int i = threadIdx.x; i < n; i += blockDim.x) counters[i] = 0u;
-    if (threadIdx.x == 0) {
-        if (done) *done = 0u;
-        if (status) *status = 0u;
-    }
+    if (threadIdx.x == 0 && done) *done = done_tag;
     if (!gate) return;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
@@ -133,7 +159,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 
 
 // Common fields of a consumer launch; the wait limit in device clock ticks.
 fo_status consume_args(const uint16_t* src, const uint16_t* peer, uint16_t* dst, const uint32_t* counter,
-                       uint32_t target, uint32_t* status, ConsumeArgs* a) {
+                       uint32_t target, uint32_t* status, const fo_options& o, ConsumeArgs* a) {
     int64_t khz = 0;
     fo_status st = clock_khz(&khz);
     if (st != FO_OK) return st;
@@ -143,7 +169,7 @@ fo_status consume_args(const uint16_t* src, const uint16_t* peer, uint16_t* dst,
     a->counter = counter;
     a->target = target;
     a->status = status;
-    a->timeout_ticks = (uint64_t)poll_timeout_us() * (uint64_t)khz / 1000u;
+    a->timeout_ticks = (uint64_t)o.poll_timeout_us * (uint64_t)khz / 1000u;
     return FO_OK;
 }
 
@@ -209,22 +235,10 @@ void fo_get_consumer_grid(int32_t* max_blocks, int32_t* threads) {
     if (threads) *threads = fo::g_consumer_threads.load();
 }
 
-fo_status fo_set_consumer_limit(int32_t max_blocks) {
+fo_status fo_options_init(fo_options* o) {
     fo::clear_error();
-    if (max_blocks < 0 || max_blocks > fo::kMaxConsumeBlocks)
-        return fo::fail(FO_ERR_ARG, "max_blocks must be 0 (no cap) or in [1, 256]");
-    fo::g_consumer_limit.store(max_blocks);
-    return FO_OK;
-}
-
-int32_t fo_get_consumer_limit(void) { return fo::g_consumer_limit.load(); }
-
-fo_status fo_set_tile_trace(uint64_t* trace, int64_t capacity_tiles) {
-    fo::clear_error();
-    if (trace && capacity_tiles < 1) return fo::fail(FO_ERR_ARG, "capacity_tiles must be >= 1");
-    if (trace && (reinterpret_cast<uintptr_t>(trace) & 7)) return fo::fail(FO_ERR_ARG, "trace must be 8-byte aligned");
-    fo::g_trace_cap.store(trace ? capacity_tiles : 0);
-    fo::g_trace.store(trace);
+    if (!o) return fo::fail(FO_ERR_ARG, "options is NULL");
+    *o = fo::defaults();
     return FO_OK;
 }
 
@@ -259,9 +273,13 @@ fo_status fo_reset_counters(uint32_t* counters, int32_t n, void* stream) {
 }
 
 fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan, const void* A,
-                                 const void* W, void* C_out, uint32_t* counters, void* stream) {
+                                 const void* W, void* C_out, uint32_t* counters, void* stream,
+                                 const fo_options* options) {
     fo::clear_error();
     if (!plan) return fo::fail(FO_ERR_ARG, "plan is NULL");
+    fo_options o;
+    fo_status st = fo::resolve(options, &o);
+    if (st != FO_OK) return st;
     if (plan->tiles == 0) return FO_OK;
     if (!A || !W || !C_out) return fo::fail(FO_ERR_ARG, "null operand");
     if (!dev_plan && (plan->pattern != FO_PATTERN_ROWMAJOR || counters))
@@ -294,10 +312,10 @@ fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan, cons
         a.pool_off = fo::dev_table<int32_t>(dev_plan, L.pool_off);
     }
     a.counters = plan->P > 0 ? counters : nullptr;
-    a.sync = fo::g_sync_producer.load(std::memory_order_relaxed);
+    a.sync = o.sync_producer;
     a.c_rsrc = plan->M * plan->N * 2 <= INT32_MAX ? 1 : 0;
-    a.trace = fo::g_trace.load(std::memory_order_relaxed);
-    a.trace_cap = a.trace ? fo::g_trace_cap.load(std::memory_order_relaxed) : 0;
+    a.trace = o.tile_trace;
+    a.trace_cap = a.trace ? o.tile_trace_capacity : 0;
     // Persistent grid: one workgroup per tile of a wave. Position classes
     // follow the chiplet of the XCD dispatch order.
     const int grid = std::min(plan->tiles, std::max(plan->W, 1));
@@ -312,22 +330,23 @@ fo_status fo_gemm_signal_reorder(const fo_plan* plan, const void* dev_plan, cons
 
 fo_status fo_consume_group(const void* src, const void* peer, void* dst, int64_t len,
                            int32_t dtype, const uint32_t* counter, uint32_t target,
-                           uint32_t* status_word, void* stream) {
+                           uint32_t* status_word, void* stream, const fo_options* options) {
     fo::clear_error();
+    fo_options o;
+    fo_status st = fo::resolve(options, &o);
+    if (st != FO_OK) return st;
     if (len < 0) return fo::fail(FO_ERR_ARG, "len < 0");
     if (dtype != FO_FP16 && dtype != FO_BF16) return fo::fail(FO_ERR_ARG, "bad dtype");
     if (len == 0 && !counter) return FO_OK;
     if (len > 0 && (!src || !dst)) return fo::fail(FO_ERR_ARG, "null src or dst");
     fo::ConsumeArgs a{};
-    fo_status st = fo::consume_args(static_cast<const uint16_t*>(src), static_cast<const uint16_t*>(peer),
-                                    static_cast<uint16_t*>(dst), counter, target, status_word, &a);
+    st = fo::consume_args(static_cast<const uint16_t*>(src), static_cast<const uint16_t*>(peer),
+                          static_cast<uint16_t*>(dst), counter, target, status_word, o, &a);
     if (st != FO_OK) return st;
     a.nseg = 1;
     a.seg[0] = fo::ConsumeSegment{0, 0, len};
-    hipError_t e = fo::launch_consume(dtype, fo::g_sync_consumer.load(std::memory_order_relaxed), a,
-                                      fo::limited(fo::g_consumer_blocks.load(std::memory_order_relaxed)),
-                                      fo::g_consumer_threads.load(std::memory_order_relaxed), false,
-                                      (hipStream_t)stream);
+    hipError_t e = fo::launch_consume(dtype, o.sync_consumer, a, fo::limited(o, o.consumer_blocks),
+                                      o.consumer_threads, false, (hipStream_t)stream);
     return e == hipSuccess ? FO_OK : fo::hip_fail("consumer launch", e);
 }
 
@@ -389,9 +408,12 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
                             void* C_out, const void* peer, void* dst, void* out, const void* bias,
                             const void* gamma, float eps, int32_t do_rmsnorm, uint32_t* counters,
                             uint32_t* status_word, void* gemm_stream, void* comm_stream,
-                            void* gemm_begin_event, void* gemm_end_event) {
+                            void* gemm_begin_event, void* gemm_end_event, const fo_options* options) {
     fo::clear_error();
     if (!plan) return fo::fail(FO_ERR_ARG, "plan is NULL");
+    fo_options o;
+    fo_status st = fo::resolve(options, &o);
+    if (st != FO_OK) return st;
     if (plan->tiles == 0) return FO_OK;
     if (!dst) return fo::fail(FO_ERR_ARG, "dst is NULL");
     // An overlapped run with one group has nothing to overlap (its consumer
@@ -404,29 +426,30 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
     // hold its reset kernel behind the gate kernel that waits for it.
     if (overlap && !gemm_stream) return fo::fail(FO_ERR_ARG, "an overlapped run needs a created GEMM stream");
     hipStream_t s1 = (hipStream_t)gemm_stream, s2 = (hipStream_t)comm_stream;
-    fo_status st;
     hipError_t e;
     fo::ConsumeArgs a{};
     // consume_args also yields the wait limit in device clock ticks
     if ((st = fo::consume_args(static_cast<const uint16_t*>(C_out), static_cast<const uint16_t*>(peer),
-                               static_cast<uint16_t*>(dst), nullptr, 0, status_word, &a)) != FO_OK)
+                               static_cast<uint16_t*>(dst), nullptr, 0, status_word, o, &a)) != FO_OK)
         return st;
     const uint64_t ticks = a.timeout_ticks;
     // Handoff words after the group and position counters.
     uint32_t* gate = overlap ? counters + plan->P + FO_DISPENSER_WORDS : nullptr;
     uint32_t* done = overlap ? gate + 1 : nullptr;
-    const uint32_t tag =
-        fo::kGateTag | (fo::g_run_seq.fetch_add(1, std::memory_order_relaxed) & (fo::kGateTimedOut - 1));
-    if (requested || status_word) {
-        hipLaunchKernelGGL(fo::reset_run_kernel, dim3(1), dim3(256), 0, s1, counters,
-                           requested ? plan->P + FO_DISPENSER_WORDS : 0, done, status_word, gate, tag);
+    const uint32_t seq = fo::g_run_seq.fetch_add(1, std::memory_order_relaxed);
+    const uint32_t tag = fo::kGateTag | (seq & fo::kGateSeqMask);
+    const uint32_t done_tag = fo::done_tag_of(seq);
+    if (requested) {
+        hipLaunchKernelGGL(fo::reset_run_kernel, dim3(1), dim3(256), 0, s1, counters, plan->P + FO_DISPENSER_WORDS,
+                           done, done_tag, status_word, gate, tag);
         if ((e = hipGetLastError()) != hipSuccess) return fo::hip_fail("reset kernel launch", e);
     }
     if (overlap && (e = fo::launch_gate(gate, tag, status_word, ticks, s2)) != hipSuccess)
         return fo::hip_fail("gate kernel launch", e);
     if (gemm_begin_event && (e = hipEventRecord((hipEvent_t)gemm_begin_event, s1)) != hipSuccess)
         return fo::hip_fail("hipEventRecord", e);
-    if ((st = fo_gemm_signal_reorder(plan, dev_plan, A, W, C_out, requested ? counters : nullptr, s1)) != FO_OK)
+    if ((st = fo_gemm_signal_reorder(plan, dev_plan, A, W, C_out, requested ? counters : nullptr, s1, &o)) !=
+        FO_OK)
         return st;
     if (gemm_end_event && (e = hipEventRecord((hipEvent_t)gemm_end_event, s1)) != hipSuccess)
         return fo::hip_fail("hipEventRecord", e);
@@ -439,9 +462,9 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
     // the post-reorder.
     const int64_t* seg = plan->segs.data();
     const int nseg = (int)(plan->segs.size() / 5);
-    const int sync = fo::g_sync_consumer.load(std::memory_order_relaxed);
-    const int cap = fo::g_consumer_blocks.load(std::memory_order_relaxed);
-    const int cap_threads = fo::g_consumer_threads.load(std::memory_order_relaxed);
+    const int sync = o.sync_consumer;
+    const int cap = o.consumer_blocks;
+    const int cap_threads = o.consumer_threads;
     struct Launch {
         fo::ConsumeArgs args;
         bool last;
@@ -463,18 +486,23 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
         fo::ConsumeArgs& c = launches[k].args;
         const bool final_launch = overlap && k + 1 == launches.size();
         c.done = final_launch ? done : nullptr;
+        c.done_tag = done_tag;
         // Under a consumer limit every launch takes the variant that runs
         // beside the GEMM, so that the emulated link has one speed in
         // overlapped and serialized runs alike.
-        const bool capped = fo::g_consumer_limit.load(std::memory_order_relaxed) > 0;
+        const bool capped = o.consumer_limit > 0;
         const bool last = launches[k].last;
-        const int blocks = fo::limited(last ? fo::kMaxConsumeBlocks : cap);
+        const int blocks = fo::limited(o, last ? fo::kMaxConsumeBlocks : cap);
         const int threads = last ? 256 : cap_threads;
         if ((e = fo::launch_consume(plan->dtype, sync, c, blocks, threads, last && !capped, overlap ? s2 : s1,
                                     final_launch ? &final_blocks : nullptr)) != hipSuccess)
             return fo::hip_fail("consumer launch", e);
     }
-    if (final_blocks > 0 && (e = fo::launch_wait(done, (uint32_t)final_blocks, status_word, ticks, s1)) != hipSuccess)
+    // the done word reaches the run's tag plus the launch's grid only through
+    // this run's final consumer (a late consumer of an earlier run finds
+    // another tag in it and does not count)
+    if (final_blocks > 0 &&
+        (e = fo::launch_wait(done, done_tag + (uint32_t)final_blocks, status_word, ticks, s1)) != hipSuccess)
         return fo::hip_fail("wait kernel launch", e);
     if (out) return fo_post_reorder(plan, dev_plan, dst, out, bias, gamma, eps, do_rmsnorm, s1);
     return FO_OK;

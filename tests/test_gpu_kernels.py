@@ -305,14 +305,10 @@ def test_tile_trace():
     ctr = zeros_u32(plan.num_counters)
     fo.gemm_signal_reorder(plan, dp, dA, dW, ref, ctr)
     trace = torch.zeros(4 * plan.tiles, dtype=torch.int64, device="cuda")
-    fo.set_tile_trace(trace, plan.tiles)
-    try:
-        C = empty16(M * N, "fp16")
-        ctr = zeros_u32(plan.num_counters)
-        fo.gemm_signal_reorder(plan, dp, dA, dW, C, ctr)
-        torch.cuda.synchronize()
-    finally:
-        fo.set_tile_trace(None)
+    C = empty16(M * N, "fp16")
+    ctr = zeros_u32(plan.num_counters)
+    fo.gemm_signal_reorder(plan, dp, dA, dW, C, ctr, opts={"tile_trace": trace, "tile_trace_capacity": plan.tiles})
+    torch.cuda.synchronize()
     np.testing.assert_array_equal(from_dev(C)[:M * N], from_dev(ref)[:M * N])
     t = trace.cpu().numpy().reshape(-1, 4)
     assert np.all(t[:, 0] > 0) and np.all(t[:, 1] >= t[:, 0])

@@ -186,17 +186,29 @@ def test_process_wide_settings_validate_and_round_trip():
             fo.set_sync_mode(3, 0)
         fo.set_sync_mode(1, 0)
         assert fo.get_sync_mode() == (1, 0)
-        for bad in (-1, 257):
-            with pytest.raises(fo.FoError) as e:
-                fo.set_consumer_limit(bad)
-            assert e.value.status == -1
-        assert fo.get_consumer_limit() == 0
-        fo.set_consumer_limit(16)
-        assert fo.get_consumer_limit() == 16
+        # per-call options start from the process defaults as they stand
+        o = fo.options()
+        assert (o.sync_producer, o.sync_consumer) == (1, 0)
+        assert (o.consumer_blocks, o.consumer_threads) == (7, 128)
+        assert o.poll_timeout_us == fo.get_poll_timeout_us() and o.consumer_limit == 0
+        assert o.tile_trace is None and o.tile_trace_capacity == 0
     finally:
         fo.set_consumer_grid(*old_grid)
         fo.set_sync_mode(*old_modes)
-        fo.set_consumer_limit(0)
+
+
+@pytest.mark.parametrize("bad", [dict(sync_producer=3), dict(sync_consumer=-1), dict(consumer_blocks=0),
+                                 dict(consumer_blocks=257), dict(consumer_threads=96),
+                                 dict(poll_timeout_us=0), dict(consumer_limit=-1), dict(consumer_limit=257),
+                                 dict(reserved0=1), dict(tile_trace=8, tile_trace_capacity=0),
+                                 dict(tile_trace=12, tile_trace_capacity=4)])
+def test_per_call_options_are_checked(bad):
+    # checked before any device work: an empty consumer call (no counter, no
+    # elements) with bad options fails, with good ones launches nothing
+    fo.consume_group(None, None, None, 0, "fp16", opts={})
+    with pytest.raises(fo.FoError) as e:
+        fo.consume_group(None, None, None, 0, "fp16", opts=bad)
+    assert e.value.status == -1
 
 
 @pytest.mark.parametrize("seed", range(4))
