@@ -314,3 +314,39 @@ def test_tile_trace():
     assert np.all(t[:, 0] > 0) and np.all(t[:, 1] >= t[:, 0])
     assert np.all((t[:, 3] >= 0) & (t[:, 3] < min(plan.tiles, plan.W)))
     assert fo.device_wall_clock_khz() > 0
+
+
+@pytest.mark.parametrize("order,tile,shape,cus", [("xcd", (256, 256), (1024, 1280, 512), 8),
+                                                  ("xcd", (256, 128), (1024, 1024, 256), 8),
+                                                  ("rowmajor", (64, 64), (256, 256, 128), 4)])
+def test_back_to_back_launches_need_no_dispenser_reset(order, tile, shape, cus):
+    # launches on one counters array whose position words are never cleared
+    # in between (only the group counters are): each launch must leave them
+    # zero (the last workgroup of each position class clears its word), so
+    # every launch computes every tile
+    torch = torch_mod()
+    M, N, K = shape
+    say(f"[gemm dispensers] order={order} tile={tile} M={M} N={N} K={K} cus={cus}")
+    A, W = _operands(M, N, K, "fp16", 31)
+    plan = fo.plan_groups(M, N, K, dtype="fp16", tile_m=tile[0], tile_n=tile[1], order=order, num_cus=cus,
+                          pattern="tile", sizes=[plan_T(M, N, tile, cus)])
+    dA, dW = to_dev(A), to_dev(W)
+    dp = dev_plan(plan)
+    ref = empty16(M * N, "fp16")
+    ctr = zeros_u32(plan.num_counters)
+    fo.gemm_signal_reorder(plan, dp, dA, dW, ref, ctr)
+    torch.cuda.synchronize()
+    assert not ctr.cpu().numpy()[plan.P:plan.P + fo.DISPENSER_WORDS].any(), "position words left non-zero"
+    for k in range(3):
+        C = empty16(M * N, "fp16")
+        ctr[:plan.P].zero_()
+        fo.gemm_signal_reorder(plan, dp, dA, dW, C, ctr)
+        torch.cuda.synchronize()
+        c = ctr.cpu().numpy()
+        np.testing.assert_array_equal(c[:plan.P], np.array(plan.targets), err_msg=f"launch {k}")
+        assert not c[plan.P:plan.P + fo.DISPENSER_WORDS].any(), f"launch {k}: position words left non-zero"
+        np.testing.assert_array_equal(from_dev(C)[:M * N], from_dev(ref)[:M * N], err_msg=f"launch {k}")
+
+
+def plan_T(M, N, tile, cus):
+    return -(-((M // tile[0]) * (N // tile[1])) // cus)
