@@ -438,6 +438,33 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan,
                             const fo_options* options);
 
 /*
+ * fo_run_overlapped_noalloc -- fo_run_overlapped for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same run, with the counters array
+ * taken from a static array of FO_NOALLOC_MAX_COUNTERS uint32 words that the
+ * library holds on every device it runs on until the process ends. The call
+ * allocates nothing and calls no allocating routine; the caller passes the
+ * inputs and outputs as for fo_run_overlapped (status_word included: it is
+ * an output, sticky as there), no events. Each run's reset kernel clears what
+ * must start at zero (the group and position counters); the gate word keeps
+ * the last run's tag. Every call on one device shares that device's array:
+ * calls that may overlap on one device (other streams, other threads) race
+ * and must not be issued; calls queued on the same pair of streams are
+ * ordered by the streams and are fine.
+ * Errors: FO_ERR_ARG when the plan needs more than FO_NOALLOC_MAX_COUNTERS
+ * counter words (fo_plan_num_counters), before any device work; FO_ERR_HIP
+ * when the array's address cannot be had; and those of fo_run_overlapped.
+ */
+#define FO_NOALLOC_MAX_COUNTERS 1024
+fo_status fo_run_overlapped_noalloc(const fo_plan* plan, const void* dev_plan,
+                                    const void* A, const void* W, void* C_out,
+                                    const void* peer, void* dst, void* out,
+                                    const void* bias, const void* gamma, float eps,
+                                    int32_t do_rmsnorm, uint32_t* status_word,
+                                    void* gemm_stream, void* comm_stream,
+                                    const fo_options* options);
+
+/*
  * How the producer (GEMM epilogue) publishes a finished tile and how the
  * consumer reads a signalled group. All modes are correct; they differ in
  * the cache maintenance they cost (MI355X has one L2 per chiplet):

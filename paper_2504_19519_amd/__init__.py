@@ -19,7 +19,7 @@ import numpy as np
 
 __all__ = [
     "FoError", "Plan", "PlanCache", "plan_groups", "gemm_signal_reorder", "consume_group",
-    "post_reorder", "reset_counters", "run_overlapped", "set_poll_timeout_us",
+    "post_reorder", "reset_counters", "run_overlapped", "run_overlapped_noalloc", "set_poll_timeout_us",
     "get_poll_timeout_us", "device_num_cus", "set_sync_mode", "get_sync_mode",
     "set_consumer_grid", "get_consumer_grid", "Options", "options", "device_wall_clock_khz", "LIB_PATH",
     "FP16", "BF16", "TILE", "SUBTILE", "SUBTOKEN", "ROWMAJOR",
@@ -120,6 +120,9 @@ def lib() -> ctypes.CDLL:
     L.fo_reset_counters.argtypes = [vp, i32, vp]
     L.fo_run_overlapped.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, i32,
                                     vp, vp, vp, vp, vp, vp, po]
+    L.fo_run_overlapped_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, i32,
+                                            vp, vp, vp, po]
+    L.fo_run_overlapped_noalloc.restype = ctypes.c_int
     L.fo_set_sync_mode.argtypes, L.fo_set_sync_mode.restype = [i32, i32], ctypes.c_int
     L.fo_get_sync_mode.argtypes = [pi32, pi32]
     L.fo_set_consumer_grid.argtypes, L.fo_set_consumer_grid.restype = [i32, i32], ctypes.c_int
@@ -469,6 +472,30 @@ def run_overlapped(plan: Plan, dev_plan, A, W, C_out, peer, dst, out=None, bias=
                                    float(eps), int(bool(do_rmsnorm)), _ptr(counters),
                                    _ptr(status_word), _stream(gemm_stream), _stream(comm_stream),
                                    _event(gemm_begin_event), _event(gemm_end_event), _opts(opts)))
+
+
+NOALLOC_MAX_COUNTERS = 1024    # FO_NOALLOC_MAX_COUNTERS
+
+
+def run_overlapped_noalloc(plan: Plan, dev_plan, A, W, C_out, peer, dst, out=None, bias=None, gamma=None,
+                           eps: float = 1e-6, do_rmsnorm: bool = False, status_word=None,
+                           gemm_stream=None, comm_stream=None, opts=None) -> None:
+    """fo_run_overlapped_noalloc: the overlapped run with the library's static
+    counters array (no device allocation; calls on one device must not
+    overlap)."""
+    _need(A, 2 * plan.M * plan.K, "A")
+    _need(W, 2 * plan.N * plan.K, "W")
+    _need(C_out, 2 * plan.M * plan.N, "C_out")
+    _need(peer, 2 * plan.M * plan.N, "peer")
+    _need(dst, 2 * plan.dest_elems, "dst")
+    _need(out, 2 * plan.M * plan.N, "out")
+    _need(bias, 2 * plan.N, "bias")
+    _need(gamma, 2 * plan.N, "gamma")
+    _need(status_word, 4, "status_word")
+    _check(lib().fo_run_overlapped_noalloc(plan.handle, _ptr(dev_plan), _ptr(A), _ptr(W), _ptr(C_out),
+                                           _ptr(peer), _ptr(dst), _ptr(out), _ptr(bias), _ptr(gamma),
+                                           float(eps), int(bool(do_rmsnorm)), _ptr(status_word),
+                                           _stream(gemm_stream), _stream(comm_stream), _opts(opts)))
 
 
 SYNC_FENCE_ALL, SYNC_FENCE_ONE, SYNC_COHERENT = 0, 1, 2

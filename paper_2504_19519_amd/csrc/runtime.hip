@@ -7,6 +7,7 @@
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -144,6 +145,30 @@ __global__ __launch_bounds__(256) void reset_run_kernel(uint32_t* counters, int3
         if (old == (tag | kGateTimedOut) && status)
             __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+}
+
+// Counters array of fo_run_overlapped_noalloc, one copy per device (a
+// file-scope device array, zero when the code object is loaded). Host code
+// never passes the array's name to a kernel: the address of this device's
+// copy comes from hipGetSymbolAddress, once per device.
+__device__ __align__(256) uint32_t scratch[FO_NOALLOC_MAX_COUNTERS];
+std::mutex g_scratch_mu;
+uint32_t* g_scratch_ptr[kMaxDevices];
+
+fo_status scratch_of_current_device(uint32_t** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail("hipGetDevice", e);
+    if (dev < 0 || dev >= kMaxDevices) return fail(FO_ERR_ARG, "device index out of range");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) return hip_fail("hipGetSymbolAddress(scratch)", e);
+        g_scratch_ptr[dev] = static_cast<uint32_t*>(p);
+    }
+    *out = g_scratch_ptr[dev];
+    return FO_OK;
 }
 
 // Tags of overlapped runs, unique per process (30 bits of sequence).
@@ -506,6 +531,27 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
         return fo::hip_fail("wait kernel launch", e);
     if (out) return fo_post_reorder(plan, dev_plan, dst, out, bias, gamma, eps, do_rmsnorm, s1);
     return FO_OK;
+}
+
+fo_status fo_run_overlapped_noalloc(const fo_plan* plan, const void* dev_plan, const void* A, const void* W,
+                                    void* C_out, const void* peer, void* dst, void* out, const void* bias,
+                                    const void* gamma, float eps, int32_t do_rmsnorm, uint32_t* status_word,
+                                    void* gemm_stream, void* comm_stream, const fo_options* options) {
+    fo::clear_error();
+    if (!plan) return fo::fail(FO_ERR_ARG, "plan is NULL");
+    const int32_t need = fo_plan_num_counters(plan);
+    if (need > FO_NOALLOC_MAX_COUNTERS)
+        return fo::fail(FO_ERR_ARG, "fo_run_overlapped_noalloc: the plan needs " + std::to_string(need) +
+                                        " counter words, the library's static array holds " +
+                                        std::to_string(FO_NOALLOC_MAX_COUNTERS));
+    fo_options o;
+    fo_status st = fo::resolve(options, &o);
+    if (st != FO_OK) return st;
+    if (plan->tiles == 0) return FO_OK;
+    uint32_t* counters = nullptr;
+    if ((st = fo::scratch_of_current_device(&counters)) != FO_OK) return st;
+    return fo_run_overlapped(plan, dev_plan, A, W, C_out, peer, dst, out, bias, gamma, eps, do_rmsnorm, counters,
+                             status_word, gemm_stream, comm_stream, nullptr, nullptr, &o);
 }
 
 }  // extern "C"

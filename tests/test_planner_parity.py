@@ -271,3 +271,14 @@ def test_binding_rejects_short_tensors_before_the_call():
         fo.consume_group(1, None, torch.zeros(7, dtype=torch.int16), 8, "fp16")
     with pytest.raises(ValueError, match="gamma"):
         fo.post_reorder(p, 1, 1, 1, gamma=torch.zeros(1023, dtype=torch.int16))
+
+
+def test_noalloc_rejects_plans_beyond_its_static_array():
+    # 1024 groups of one 64x64 tile need 1024 + 10 counter words: refused
+    # before any device work, with the limit in the message
+    plan = fo.plan_groups(2048, 2048, 64, dtype="fp16", tile_m=64, tile_n=64, order="rowmajor", num_cus=256,
+                          pattern="tile", sizes=[1] * 1024, unit="tiles")
+    assert plan.num_counters > fo.NOALLOC_MAX_COUNTERS
+    with pytest.raises(fo.FoError) as e:
+        fo.run_overlapped_noalloc(plan, 16, 16, 16, 16, None, 16, None)
+    assert e.value.status == -1 and str(fo.NOALLOC_MAX_COUNTERS) in str(e.value)
