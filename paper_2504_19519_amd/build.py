@@ -58,10 +58,12 @@ def _resource_usage(text: str) -> dict:
             name = m.group(1)
             out[name] = {}
             continue
-        m = re.search(r"remark:\s+(VGPRs|AGPRs|VGPRs Spill|LDS Size \[bytes/block\]|Occupancy \[waves/SIMD\]): (\d+)", line)
+        m = re.search(r"remark:\s+(VGPRs|AGPRs|VGPRs Spill|ScratchSize \[bytes/lane\]|LDS Size \[bytes/block\]|"
+                      r"Occupancy \[waves/SIMD\]): (\d+)", line)
         if m and name:
             key = {"VGPRs": "vgpr", "AGPRs": "agpr", "VGPRs Spill": "vgpr_spill",
-                   "LDS Size [bytes/block]": "lds", "Occupancy [waves/SIMD]": "occupancy"}[m.group(1)]
+                   "ScratchSize [bytes/lane]": "scratch", "LDS Size [bytes/block]": "lds",
+                   "Occupancy [waves/SIMD]": "occupancy"}[m.group(1)]
             out[name][key] = int(m.group(2))
     return out
 

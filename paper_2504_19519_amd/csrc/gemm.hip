@@ -7,14 +7,24 @@
 // of one tile per compute unit (Section 2.1.1) and position p is the tile's
 // slot in the reordered output (Section 3.3 Approach (1)).
 //
-// Main loop: MFMA v_mfma_f32_32x32x16 (fp16 / bf16 in, fp32 accumulate) on
-// k steps of 64, 4 or 8 waves of 128 x 64 (or 32 x 32) each. A and W tiles move from
-// memory straight into an LDS ring of STAGES stages (direct global-to-LDS
-// loads, XOR-swizzled rows for conflict-free 16-byte fragment reads), issued
-// STAGES steps ahead; fragments of the next 16-wide k step are read while the
-// MFMAs of the current one run, and every LDS read and load issue sits in the
-// shadow of an MFMA. The main loop is the same for every output pattern
-// (Section 5: only the epilogue changes).
+// Main loop, k steps of 64, A and W tiles moving from memory straight into an
+// LDS ring of STAGES stages (direct global-to-LDS loads, XOR-swizzled rows for
+// conflict-free 16-byte fragment reads); fragments of the next MFMA k step are
+// read while the MFMAs of the current one run, and every LDS read and load
+// issue sits in the shadow of an MFMA. Two forms:
+//   256x256 tiles: 4 waves of 128 x 128 (one per SIMD), v_mfma_f32_16x16x32
+//     in inline asm with the accumulators tied in place (mostly AGPRs), two
+//     stages; a wave reads 2/3 of the LDS bytes per flop that 8 waves of
+//     128 x 64 read, which lets the power-limited clock run higher. A
+//     substep's 64 MFMAs carry the 16 fragment reads of the next substep and,
+//     after the step's barrier, the 16 load issues of the stage just freed,
+//     one every 4 MFMAs (bunched issues stall the single wave of a SIMD on
+//     the memory pipeline).
+//   256x128 and 64x64 tiles: 8 (or 4) waves of 64 x 64 (32 x 32),
+//     v_mfma_f32_32x32x16 from the compiler's builtin, loads issued STAGES
+//     steps ahead.
+// The main loop is the same for every output pattern (Section 5: only the
+// epilogue changes).
 //
 // Epilogue (Section 3.3 Approach; Section 3.2 Approach):
 //   1. accumulators -> fp16/bf16 (round to nearest even) -> LDS staging tile
@@ -29,6 +39,7 @@
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
+#include <utility>
 
 #include "fo_device.h"
 #include "fo_internal.h"
@@ -49,6 +60,48 @@ constexpr int kRsrcWord3 = 0x00020000;
 constexpr int kCachePolicySc1 = 16;
 
 typedef __attribute__((address_space(3))) void lds_void_t;
+
+// 16x16x32 MFMA in inline asm with the accumulator tied in place (dst =
+// srcC): with 256 accumulator registers per wave the compiler's own MFMAs
+// get copied between register files every step. KEEP_V: the accumulator is
+// held in VGPRs instead of AGPRs. The compiler does not track the hazards of
+// these instructions: accumulators are never written by VALU right before
+// one (the first MFMA of a tile takes srcC = 0 instead of a zeroed
+// accumulator) and are read only after the wait that ends the main loop.
+template <int DT, bool KEEP_V, typename C>
+__device__ __forceinline__ void mfma16_tied(C& c, const u32x4_t& a, const u32x4_t& b) {
+    if constexpr (DT == FO_FP16 && KEEP_V)
+        asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(b));
+    else if constexpr (DT == FO_FP16)
+        asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+    else if constexpr (KEEP_V)
+        asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(b));
+    else
+        asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+}
+// The same with srcC = 0: the first MFMA of a tile starts its accumulator.
+template <int DT, bool KEEP_V, typename C>
+__device__ __forceinline__ void mfma16_first(C& c, const u32x4_t& a, const u32x4_t& b) {
+    if constexpr (DT == FO_FP16 && KEEP_V)
+        asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, 0" : "=v"(c) : "v"(a), "v"(b));
+    else if constexpr (DT == FO_FP16)
+        asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, 0" : "=a"(c) : "v"(a), "v"(b));
+    else if constexpr (KEEP_V)
+        asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=v"(c) : "v"(a), "v"(b));
+    else
+        asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=a"(c) : "v"(a), "v"(b));
+}
+
+// Calls f(std::integral_constant<int, I>{}) for I = 0 .. N-1 (indices known
+// at compile time, so the arrays they index stay in registers).
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+    (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 template <int DT>
 __device__ __forceinline__ f32x16_t mfma32(u32x4_t a, u32x4_t b, f32x16_t c) {
@@ -98,7 +151,7 @@ struct Tiles {
 // w_bytes long; the host checks they fit in 32 bits): a read past them
 // returns zero instead of faulting, and a resource of length 0 loads zeros
 // without touching memory.
-template <int AI, int BI, int KA>
+template <int AI, int BI, int KA, bool OPAQUE = true>
 __device__ __forceinline__ void issue_tile(const uint16_t* Ablk, const uint16_t* Wblk, uint32_t a_bytes,
                                            uint32_t w_bytes, const uint32_t* voffA, const uint32_t* voffB,
                                            uint32_t soff, char* st, int wave) {
@@ -108,9 +161,11 @@ __device__ __forceinline__ void issue_tile(const uint16_t* Ablk, const uint16_t*
         __builtin_amdgcn_make_buffer_rsrc((void*)Wblk, 0, (int)w_bytes, kRsrcWord3);
     // The LDS block addresses (one scalar register each, M0 of the load) are
     // formed here from an opaque copy of the wave index, so that they are
-    // not all kept live through the main loop.
+    // not all kept live through the main loop (OPAQUE; the 4-wave kernel
+    // takes the uniform index directly).
     int w = wave;
-    asm volatile("" : "+s"(w));
+    if constexpr (OPAQUE) asm volatile("" : "+s"(w));
+    else w = __builtin_amdgcn_readfirstlane(wave);
 #pragma unroll
     for (int i = 0; i < AI; ++i)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void_t*)(st + (w * AI + i) * 1024), 16, voffA[i],
@@ -119,6 +174,24 @@ __device__ __forceinline__ void issue_tile(const uint16_t* Ablk, const uint16_t*
     for (int i = 0; i < BI; ++i)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rW, (lds_void_t*)(st + KA + (w * BI + i) * 1024), 16,
                                                  voffB[i], soff, 0, 0);
+}
+
+// Load instruction idx (0 .. AI + BI - 1) of issue_tile alone, so that a
+// step's loads can be spread over its MFMAs.
+template <int AI, int BI, int KA>
+__device__ __forceinline__ void issue_one(int idx, const uint16_t* Ablk, const uint16_t* Wblk, uint32_t a_bytes,
+                                          uint32_t w_bytes, const uint32_t* voffA, const uint32_t* voffB,
+                                          uint32_t soff, char* st, int wave) {
+    const int w = __builtin_amdgcn_readfirstlane(wave);
+    if (idx < AI) {
+        const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc((void*)Ablk, 0, (int)a_bytes, kRsrcWord3);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void_t*)(st + (w * AI + idx) * 1024), 16, voffA[idx], soff,
+                                                 0, 0);
+    } else {
+        const __amdgpu_buffer_rsrc_t rW = __builtin_amdgcn_make_buffer_rsrc((void*)Wblk, 0, (int)w_bytes, kRsrcWord3);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rW, (lds_void_t*)(st + KA + (w * BI + idx - AI) * 1024), 16,
+                                                 voffB[idx - AI], soff, 0, 0);
+    }
 }
 
 // Instruction order inside one k-step phase of the main loop: each MFMA
@@ -152,17 +225,25 @@ __device__ __forceinline__ void wait_and_barrier() {
     asm volatile("" ::: "memory");
 }
 
-template <int DT, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int BK>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(const GemmArgs a) {
+// The kernel body; MF = 32 (v_mfma_f32_32x32x16, compiler builtin) or 16
+// (v_mfma_f32_16x16x32 in tied inline asm, two stages of 64-wide k steps).
+template <int DT, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int BK, int MF>
+__device__ __forceinline__ void gemm_body(const GemmArgs& a) {
     constexpr int NW = WAVES_M * WAVES_N, NT = 64 * NW;
     constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
-    constexpr int MI = WTM / 32, NJ = WTN / 32;
+    constexpr int MI = WTM / MF, NJ = WTN / MF;
+    constexpr int KPM = 512 / MF;                        // k per MFMA: 16 (32x32) or 32 (16x16)
+    using AccT = typename std::conditional<MF == 32, f32x16_t, f32x4_t>::type;
+    constexpr int NACC = MF == 32 ? 16 : 4;              // accumulator registers per block and lane
+    constexpr int kVRows = MF == 16 ? 2 : 0;             // accumulator block rows held in VGPRs
     using T = Tiles<BM, BN, STAGES, NW, BK>;
     constexpr int kBK = T::kBK;
-    constexpr int P = kBK / 16;                          // MFMA k steps per main-loop step
+    constexpr int P = kBK / KPM;                         // MFMA k steps per main-loop step
     static_assert(NW == 4 || NW == 8, "four or eight waves");
     static_assert(NT >= BM, "one thread per tile row in the epilogue set-up");
-    static_assert(WTM % 32 == 0 && WTN % 32 == 0, "32x32 MFMA blocks");
+    static_assert(MF == 32 || MF == 16, "32x32x16 or 16x16x32 MFMAs");
+    static_assert(WTM % MF == 0 && WTN % MF == 0, "whole MFMA blocks");
+    static_assert(MF == 32 || (STAGES == 2 && P == 2), "the 16x16x32 form runs two stages of 64-wide k steps");
     static_assert(STAGES >= 2 && STAGES <= 4, "two to four LDS stages");
     static_assert(BK == 32 || BK == 64, "k steps of 32 or 64");
     static_assert(T::kAI >= 1 && T::kBI >= 1 && T::kA % (1024 * NW) == 0 && T::kB % (1024 * NW) == 0,
@@ -241,23 +322,23 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
     // same loads and the wait counts stay uniform (no branches).
     auto issue = [&](int kt, char* st) {
         const bool live = kt < KT;
-        issue_tile<T::kAI, T::kBI, T::kA>(Ablk, Wblk, live ? (uint32_t)(BM * K * 2) : 0u,
+        issue_tile<T::kAI, T::kBI, T::kA, MF == 32>(Ablk, Wblk, live ? (uint32_t)(BM * K * 2) : 0u,
                                          live ? (uint32_t)(BN * K * 2) : 0u, voffA, voffB,
                                          live ? (uint32_t)kt * (kBK * 2) : 0u, st, wave);
     };
 
-    f32x16_t acc[MI][NJ];
+    AccT acc[MI][NJ];
 
-    // Fragment addressing: lane l feeds row (l % 32) of a 32-row block with
-    // the 8 consecutive k values of chunk 2*kk + l/32 of the 16-wide step kk
-    // (32-row blocks start on multiples of 32, so the row's swizzle depends
-    // on l only).
-    const int a_row = (wm * WTM + (lane & 31)) * T::kRow;
-    const int b_row = T::kA + (wn * WTN + (lane & 31)) * T::kRow;
+    // Fragment addressing: lane l feeds row (l % MF) of an MF-row block with
+    // the 8 consecutive k values of chunk (KPM/8)*kk + l/MF of MFMA k step kk
+    // (blocks start on multiples of MF, so the row's swizzle depends on l
+    // only).
+    const int a_row = (wm * WTM + (lane & (MF - 1))) * T::kRow;
+    const int b_row = T::kA + (wn * WTN + (lane & (MF - 1))) * T::kRow;
     int cslot[P];
 #pragma unroll
     for (int kk = 0; kk < P; ++kk)
-        cslot[kk] = 16 * ((2 * kk + (lane >> 5)) ^ ((lane >> T::kSwz) & (T::kCh - 1)));
+        cslot[kk] = 16 * (((KPM / 8) * kk + lane / MF) ^ ((lane >> T::kSwz) & (T::kCh - 1)));
 
     // Two fragment register sets: the fragments of k step kk+1 are read from
     // LDS while the MFMAs of k step kk run.
@@ -265,19 +346,21 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
     auto load_frags = [&](const char* st, int kk, u32x4_t (&fa)[MI], u32x4_t (&fb)[NJ]) {
 #pragma unroll
         for (int i = 0; i < MI; ++i)
-            fa[i] = *reinterpret_cast<const u32x4_t*>(st + a_row + i * 32 * T::kRow + cslot[kk]);
+            fa[i] = *reinterpret_cast<const u32x4_t*>(st + a_row + i * MF * T::kRow + cslot[kk]);
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
-            fb[j] = *reinterpret_cast<const u32x4_t*>(st + b_row + j * 32 * T::kRow + cslot[kk]);
+            fb[j] = *reinterpret_cast<const u32x4_t*>(st + b_row + j * MF * T::kRow + cslot[kk]);
     };
-    // W fragment as the MFMA's first operand: the 32x32 result block is C^T,
-    // so each lane holds 4 consecutive output columns.
+    // W fragment as the MFMA's first operand: the result block is C^T, so
+    // each lane holds 4 consecutive output columns.
     auto mma = [&](const u32x4_t (&fa)[MI], const u32x4_t (&fb)[NJ]) {
+        if constexpr (MF == 32) {
 #pragma unroll
-        for (int i = 0; i < MI; ++i)
+            for (int i = 0; i < MI; ++i)
 #pragma unroll
-            for (int j = 0; j < NJ; ++j)
-                acc[i][j] = mfma32<DT>(fb[j], fa[i], acc[i][j]);
+                for (int j = 0; j < NJ; ++j)
+                    acc[i][j] = mfma32<DT>(fb[j], fa[i], acc[i][j]);
+        }
     };
 
     constexpr int kMfma = MI * NJ, kReads = MI + NJ;
@@ -295,7 +378,56 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
     // up to kt+STAGES-1 may still be loading): after the barrier, tile
     // kt+STAGES goes into `cur`, and the first fragments of tile kt+1 are read
     // while the last MFMAs of tile kt run.
-    auto step = [&](int kt, char* cur, const char* nxt, auto first_c) {
+    // 16x16x32 form: MFMA m of a substep (block row m / NJ, column m % NJ)
+    // carries fragment read m of the next substep (m < MI + NJ: A0, B0 ..
+    // B(NJ-1), A1 .. A(MI-1), the order the next substep needs them) and, in
+    // the substep after the barrier, every 4th MFMA one load issue of the
+    // stage just freed (step lkt; `loads`). sched_barrier keeps this order.
+    // The first substep of a tile (FIRST) starts the accumulators.
+    auto mma_rd = [&](const u32x4_t (&fa)[MI], const u32x4_t (&fb)[NJ], const char* rst, int rkk,
+                      u32x4_t (&ra)[MI], u32x4_t (&rb)[NJ], int lkt, char* lst, bool loads,
+                      auto first_c) __attribute__((always_inline)) {
+        const bool live = lkt < KT;
+        const uint32_t ab = live ? (uint32_t)(BM * K * 2) : 0u, wb = live ? (uint32_t)(BN * K * 2) : 0u;
+        const uint32_t so = live ? (uint32_t)lkt * (kBK * 2) : 0u;
+        constexpr int kGap = 4;
+        static_assert(MI * NJ >= kGap * T::kLoads, "a load issue every 4 MFMAs");
+        static_for<MI * NJ>([&](auto mc) __attribute__((always_inline)) {
+            constexpr int m = decltype(mc)::value;
+            constexpr int i = m / NJ, j = m % NJ;
+            if constexpr (m < MI + NJ) {
+                if constexpr (m == 0)
+                    ra[0] = *reinterpret_cast<const u32x4_t*>(rst + a_row + cslot[rkk]);
+                else if constexpr (m <= NJ)
+                    rb[m - 1] = *reinterpret_cast<const u32x4_t*>(rst + b_row + (m - 1) * MF * T::kRow + cslot[rkk]);
+                else
+                    ra[m - NJ] = *reinterpret_cast<const u32x4_t*>(rst + a_row + (m - NJ) * MF * T::kRow + cslot[rkk]);
+            }
+            if constexpr (m % kGap == 0 && m / kGap < T::kLoads)
+                if (loads)
+                    issue_one<T::kAI, T::kBI, T::kA>(m / kGap, Ablk, Wblk, ab, wb, voffA, voffB, so, lst, wave);
+            constexpr bool kV = i >= MI - kVRows;
+            if constexpr (decltype(first_c)::value) mfma16_first<DT, kV>(acc[i][j], fb[j], fa[i]);
+            else mfma16_tied<DT, kV>(acc[i][j], fb[j], fa[i]);
+            __builtin_amdgcn_sched_barrier(0);
+        });
+    };
+    auto step = [&](int kt, char* cur, const char* nxt, auto first_c) __attribute__((always_inline)) {
+        if constexpr (MF == 16) {
+            mma_rd(fa0, fb0, cur, 1, fa1, fb1, 0, cur, false, first_c);
+            wait_and_barrier<0>();
+            if constexpr (decltype(first_c)::value) {
+                // the previous tile's stores are complete in every wave (this
+                // barrier follows a vmcnt(0) wait): its deferred count goes out
+                if (pend >= 0) {
+                    if (tid == 0)
+                        __hip_atomic_fetch_add(a.counters + pend, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    pend = -1;
+                }
+            }
+            mma_rd(fa1, fb1, nxt, 0, fa0, fb0, kt + STAGES, cur, true, std::false_type{});
+            return;
+        }
         load_frags(cur, 1, fa1, fb1);
         mma(fa0, fb0);
         interleave_phase<kMfma, kReads, 0>();
@@ -353,12 +485,14 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
             rank = a.row_rank[tm * BM + tid];
         }
 
+        if constexpr (MF == 32) {      // (the 16x16x32 form starts them with srcC = 0)
 #pragma unroll
-        for (int i = 0; i < MI; ++i)
+            for (int i = 0; i < MI; ++i)
 #pragma unroll
-            for (int j = 0; j < NJ; ++j)
+                for (int j = 0; j < NJ; ++j)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+                    for (int r = 0; r < NACC; ++r) acc[i][j][r] = 0.0f;
+        }
 
         issue(0, st0);
         issue(1, st1);
@@ -394,6 +528,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
             }
             if (kt < KT) step(kt, st1, st0, kNo);
         }
+        // inline-asm MFMAs: the accumulators are read only once the last
+        // MFMA's result is written (the compiler inserts no wait for them)
+        if constexpr (MF == 16) asm volatile("s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7" ::: "memory");
         wait_and_barrier<0>();    // no load may still be writing LDS
         __syncthreads();          // operand stages are reused for the output tile
 
@@ -440,12 +577,12 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
             if (wm_e * WTM >= r0 && wm_e * WTM < r0 + T::kRowsPerPass) {
 #pragma unroll
                 for (int i = 0; i < MI; ++i) {
-                    const int m = wm_e * WTM - r0 + i * 32 + (lane_e & 31);
+                    const int m = wm_e * WTM - r0 + i * MF + (lane_e & (MF - 1));
 #pragma unroll
                     for (int j = 0; j < NJ; ++j) {
 #pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            const int n = wn_e * WTN + j * 32 + q * 8 + (lane_e >> 5) * 4;
+                        for (int q = 0; q < NACC / 4; ++q) {
+                            const int n = wn_e * WTN + j * MF + q * 8 + (lane_e / MF) * 4;
                             u32x2_t v;
                             v[0] = pack2<DT>(acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]);
                             v[1] = pack2<DT>(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
@@ -566,8 +703,28 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_signal_kernel(
 }
 
 template <int DT, int BM, int BN, int WM, int WN, int ST, int BK>
+__global__ __launch_bounds__(64 * WM * WN, 1) void gemm_signal_kernel(const GemmArgs a) {
+    gemm_body<DT, BM, BN, WM, WN, ST, BK, 32>(a);
+}
+
+// 256x256 tiles, 4 waves of 128x128 (16x16x32 MFMAs). At most 216 VGPRs
+// (two accumulator block rows among them, the rest of the accumulators in
+// AGPRs): the wave leaves 64 of the SIMD's 512 registers per lane to a
+// consumer wave, which can therefore run beside it.
+template <int DT>
+__global__ __launch_bounds__(256, 1) __attribute__((amdgpu_num_vgpr(216))) void gemm_w4_kernel(const GemmArgs a) {
+    gemm_body<DT, 256, 256, 2, 2, 2, 64, 16>(a);
+}
+
+template <int DT, int BM, int BN, int WM, int WN, int ST, int BK>
 hipError_t launch_t(const GemmArgs& a, int grid, hipStream_t s) {
     hipLaunchKernelGGL((gemm_signal_kernel<DT, BM, BN, WM, WN, ST, BK>), dim3(grid), dim3(64 * WM * WN), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int DT>
+hipError_t launch_w4(const GemmArgs& a, int grid, hipStream_t s) {
+    hipLaunchKernelGGL((gemm_w4_kernel<DT>), dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
@@ -578,8 +735,7 @@ hipError_t launch_gemm(int dtype, int tile_m, int tile_n, const GemmArgs& a, int
         return dtype == FO_FP16 ? launch_t<FO_FP16, 256, 128, 4, 2, 3, 64>(a, grid, s)
                                 : launch_t<FO_BF16, 256, 128, 4, 2, 3, 64>(a, grid, s);
     if (tile_m == 256 && tile_n == 256)
-        return dtype == FO_FP16 ? launch_t<FO_FP16, 256, 256, 2, 4, 2, 64>(a, grid, s)
-                                : launch_t<FO_BF16, 256, 256, 2, 4, 2, 64>(a, grid, s);
+        return dtype == FO_FP16 ? launch_w4<FO_FP16>(a, grid, s) : launch_w4<FO_BF16>(a, grid, s);
     if (tile_m == 64 && tile_n == 64)
         return dtype == FO_FP16 ? launch_t<FO_FP16, 64, 64, 2, 2, 3, 64>(a, grid, s)
                                 : launch_t<FO_BF16, 64, 64, 2, 2, 3, 64>(a, grid, s);

@@ -82,7 +82,7 @@ def summarize(out_dir: str, workload: str, phase: str, sizes: str, summary: str,
             avg = float(r["AverageNs"]) / 1e3
             lines.append(f"| {k} | {r['Calls']} | {avg:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
                          f"{float(r['MaxNs']) / 1e3:.2f} |")
-            if "gemm_signal_kernel" in k:
+            if "gemm_signal_kernel" in k or "gemm_w4_kernel" in k:
                 gemm_avg, gemm_name = avg, k
     # The step phase runs warmup + timed + instrumented passes; bench.py's
     # live GEMM figure is the average over the instrumented pass, so the

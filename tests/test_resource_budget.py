@@ -28,20 +28,30 @@ def _usage():
         return json.load(f)
 
 
+def _regs(v):
+    """Registers per lane of one wave: the VGPRs (rounded up to the 4 at which
+    the accumulation registers start) followed by the AGPRs, rounded to 8."""
+    return _round8((v["vgpr"] + 3) // 4 * 4 + v.get("agpr", 0))
+
+
 def test_consumer_fits_beside_every_gemm_kernel():
     u = _usage()
-    gemm = {k: v for k, v in u.items() if "gemm_signal_kernel" in k}
+    gemm = {k: v for k, v in u.items() if "gemm_signal_kernel" in k or "gemm_w4_kernel" in k}
     cons = {k: v for k, v in u.items() if "consume_kernel" in k}
     assert len(gemm) >= 6 and len(cons) >= 8
-    c_regs = max(_round8(v["vgpr"] + v.get("agpr", 0)) for v in cons.values())
+    c_regs = max(_regs(v) for v in cons.values())
     c_lds = max(v["lds"] for v in cons.values())
     for name, v in gemm.items():
-        assert v.get("vgpr_spill", 0) == 0, name
-        # waves of one GEMM workgroup per SIMD (template arguments: dtype,
-        # tile_m, tile_n, waves_m, waves_n, stages, k step): 4 waves -> 1, 8 -> 2
-        m = re.search(r"gemm_signal_kernelILi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)E", name)
-        assert m, name
-        per_simd = (int(m.group(4)) * int(m.group(5)) + 3) // 4
-        regs = per_simd * _round8(v["vgpr"] + v.get("agpr", 0))
+        # register spills may only go to other registers (no scratch memory)
+        assert v.get("scratch", 0) == 0, name
+        if "gemm_w4_kernel" in name:
+            per_simd = 1                   # 4 waves of 128 x 128: one per SIMD
+        else:
+            # waves of one GEMM workgroup per SIMD (template arguments: dtype,
+            # tile_m, tile_n, waves_m, waves_n, stages, k step): 4 waves -> 1, 8 -> 2
+            m = re.search(r"gemm_signal_kernelILi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)E", name)
+            assert m, name
+            per_simd = (int(m.group(4)) * int(m.group(5)) + 3) // 4
+        regs = per_simd * _regs(v)
         assert regs + c_regs <= 512, (name, regs, c_regs)
         assert v["lds"] + c_lds <= 160 * 1024, (name, v["lds"], c_lds)
