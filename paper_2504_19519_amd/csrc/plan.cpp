@@ -60,22 +60,27 @@ double range_bytes(const fo_plan& p, int32_t f0, int32_t f1, bool all_dest) {
     return (double)(f1 - f0) * p.tile_m * p.tile_n * eb;
 }
 
-// Algorithm 1: predicted overlapped latency of one candidate.
+// Predicted overlapped latency of one partition (Section 4.1, the estimate
+// Algorithm 1 ranks candidates by): the GEMM's time is spread evenly over
+// its waves, so group g's computation is done at C_g, the time of the waves
+// up to and including g; its communication starts once that computation and
+// the previous group's communication are both done, and takes the curve's
+// latency for the group's bytes: E_g = max(C_g, E_(g-1)) + comm(g), with
+// E_(-1) = 0. The partition's latency is the last group's E.
 double predict(const fo_plan& p, const std::vector<int32_t>& sizes, double gemm_us,
                const fo_grouping& g, std::vector<int32_t>& first_scratch) {
     firsts_from_waves(sizes, p.W, p.tiles, first_scratch);
-    double acc_p = 0.0, acc_m = 0.0;
     auto comm = [&](size_t j) {
         return interp_latency(g.curve_bytes, g.curve_us, g.curve_len,
                               range_bytes(p, first_scratch[j], first_scratch[j + 1], g.all_dest_bytes != 0));
     };
-    for (size_t i = 0; i < sizes.size(); ++i) {
-        const double t_m = i > 0 ? comm(i - 1) : 0.0;
-        const double t_p = gemm_us / p.T * sizes[i];
-        acc_m = std::max(acc_p, acc_m) + t_m;
-        acc_p += t_p;
+    double compute_done = 0.0;   // C_g
+    double comm_done = 0.0;      // E_(g-1), then E_g
+    for (size_t j = 0; j < sizes.size(); ++j) {
+        compute_done += gemm_us / p.T * sizes[j];
+        comm_done = std::max(compute_done, comm_done) + comm(j);
     }
-    return std::max(acc_p, acc_m) + comm(sizes.size() - 1);
+    return comm_done;
 }
 
 fo_status check_curve(const fo_grouping& g) {
