@@ -57,16 +57,15 @@ __device__ __forceinline__ uint32_t from_f32(float x) {
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
-// Two fp32 values rounded and packed into one 32-bit word (low = a); bf16
-// pairs take one v_cvt_pk_bf16_f32.
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 values rounded (to nearest even) and packed into one 32-bit word
+// (low = a): one v_cvt_pk_f16_f32 or v_cvt_pk_bf16_f32.
 template <int DT>
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
-    if constexpr (DT == 0) {
-        return from_f32<DT>(a) | (from_f32<DT>(b) << 16);
-    } else {
-        const f32x2_t v = {a, b};
-        return bit_cast<uint32_t>(__builtin_convertvector(v, bf16x2_t));
-    }
+    const f32x2_t v = {a, b};
+    if constexpr (DT == 0) return bit_cast<uint32_t>(__builtin_convertvector(v, f16x2_t));
+    else return bit_cast<uint32_t>(__builtin_convertvector(v, bf16x2_t));
 }
 
 }  // namespace fo

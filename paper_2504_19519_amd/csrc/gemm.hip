@@ -27,6 +27,9 @@
 // epilogue changes).
 //
 // Epilogue (Section 3.3 Approach; Section 3.2 Approach):
+//   0. (256x256 form) each row's destination is looked up while the tile's
+//      main loop runs, and the next position is claimed a few k steps
+//      before its end;
 //   1. accumulators -> fp16/bf16 (round to nearest even) -> LDS staging tile
 //      (in two passes of half the rows when the tile does not fit);
 //   2. every tile row goes out as full-row stores to its destination:
@@ -364,6 +367,11 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& a) {
     };
 
     constexpr int kMfma = MI * NJ, kReads = MI + NJ;
+    // 16x16x32 form: destination of tile row `tid` (element offset), looked
+    // up at the start of the tile and written to row_off after the first
+    // main-loop barrier, so that the lookups' latency hides under the loop
+    // (the previous tile's epilogue is done with row_off by then).
+    int64_t my_off = 0;
     // Group of the previous tile whose count is still to be sent (or -1):
     // with device-coherent stores and two stages, a tile's count goes out at
     // the first main-loop barrier of the workgroup's next tile, so that the
@@ -424,6 +432,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& a) {
                         __hip_atomic_fetch_add(a.counters + pend, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     pend = -1;
                 }
+                if (tid < BM) row_off[tid] = my_off;
             }
             mma_rd(fa1, fb1, nxt, 0, fa0, fb0, kt + STAGES, cur, true, std::false_type{});
             return;
@@ -485,6 +494,26 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& a) {
             rank = a.row_rank[tm * BM + tid];
         }
 
+        // Destination (element offset) of row r of the tile, by pattern.
+        auto row_dest = [&](int r) -> int64_t {
+            int64_t off;
+            if (a.pattern == FO_PATTERN_ROWMAJOR) {
+                off = ((int64_t)tm * BM + r) * a.N + (int64_t)tn * BN;
+            } else if (a.pattern == FO_PATTERN_TILE) {
+                off = ((int64_t)slot * BM + r) * BN;
+            } else if (a.pattern == FO_PATTERN_SUBTILE) {
+                const int h = BM / a.num_dest;
+                const int k = r / h, rr = r - (r / h) * h;
+                const int j = a.slot_group[slot];
+                const int64_t f0 = a.group_first[j];
+                const int64_t nj = a.group_first[j + 1] - f0;
+                off = f0 * BM * BN + ((int64_t)k * nj + (slot - f0)) * h * BN + (int64_t)rr * BN;
+            } else {
+                const int B = a.num_dest;
+                off = ((int64_t)a.pool_off[bucket] + a.pool_base[(int64_t)slot * B + bucket] + rank) * BN;
+            }
+            return off;
+        };
         if constexpr (MF == 32) {      // (the 16x16x32 form starts them with srcC = 0)
 #pragma unroll
             for (int i = 0; i < MI; ++i)
@@ -496,11 +525,15 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& a) {
 
         issue(0, st0);
         issue(1, st1);
+        if constexpr (MF == 16)
+            if (tid < BM) my_off = row_dest(tid);
         if constexpr (STAGES >= 3) issue(2, st2);
         if constexpr (STAGES >= 4) issue(3, st3);
         wait_and_barrier<(STAGES - 1) * T::kLoads>();
         load_frags(st0, 0, fa0, fb0);
         int kt = 0;
+        bool claimed = false;
+        int next = p + (int)gridDim.x;
         if constexpr (STAGES == 4) {
             for (; kt + 4 <= KT; kt += 4) {      // tile t lives in stage t % 4
                 step(kt, st0, st1, kNo);
@@ -523,6 +556,13 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& a) {
             // the first step sends the previous tile's deferred count
             step(0, st0, st1, kYes);
             for (kt = 1; kt + 2 <= KT; kt += 2) {
+                // 16x16x32 form: the next position is claimed two to three
+                // steps before the end of this tile, so that the atomic's
+                // latency hides under them
+                if (MF == 16 && a.dispenser && !claimed && kt + 4 >= KT) {
+                    claimed = true;
+                    if (tid == 0) next = claim();
+                }
                 step(kt, st1, st0, kNo);
                 step(kt + 1, st0, st1, kNo);
             }
@@ -544,37 +584,47 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& a) {
         const int lane_e = tid_e & 63, wave_e = __builtin_amdgcn_readfirstlane(tid_e >> 6);
         const int wm_e = wave_e / WAVES_N, wn_e = wave_e % WAVES_N;
         // Destination of row `tid` of the tile, by pattern.
-        if (tid < BM) {
-            const int r = tid;
-            int64_t off;
-            if (a.pattern == FO_PATTERN_ROWMAJOR) {
-                off = ((int64_t)tm * BM + r) * a.N + (int64_t)tn * BN;
-            } else if (a.pattern == FO_PATTERN_TILE) {
-                off = ((int64_t)slot * BM + r) * BN;
-            } else if (a.pattern == FO_PATTERN_SUBTILE) {
-                const int h = BM / a.num_dest;
-                const int k = r / h, rr = r - (r / h) * h;
-                const int j = a.slot_group[slot];
-                const int64_t f0 = a.group_first[j];
-                const int64_t nj = a.group_first[j + 1] - f0;
-                off = f0 * BM * BN + ((int64_t)k * nj + (slot - f0)) * h * BN + (int64_t)rr * BN;
-            } else {
-                const int B = a.num_dest;
-                off = ((int64_t)a.pool_off[bucket] + a.pool_base[(int64_t)slot * B + bucket] + rank) * BN;
-            }
-            row_off[r] = off;
-        }
+        if (MF != 16 && tid < BM) row_off[tid] = row_dest(tid);
 
-        // The next position is claimed now; the atomic's latency hides
-        // behind this tile's stores.
-        int next = p + (int)gridDim.x;
-        if (a.dispenser && tid == 0) next = claim();
+        // Otherwise the next position is claimed now; the atomic's latency
+        // hides behind this tile's stores.
+        if (a.dispenser && !claimed && tid == 0) next = claim();
 
 #pragma unroll
         for (int pass = 0; pass < T::kPasses; ++pass) {
             const int r0 = pass * T::kRowsPerPass;
             // accumulators of the waves whose rows are in this pass -> staging
-            if (wm_e * WTM >= r0 && wm_e * WTM < r0 + T::kRowsPerPass) {
+            if constexpr (MF == 16) {
+                // 256 x 256 tile, 4 waves of 128 x 128, one pass: the
+                // addresses of cptr in closed form. Lane l of block (i, j)
+                // holds tile row wm*128 + i*16 + l%16, columns wn*128 + j*16 +
+                // 4*(l/16) .. +3: staging row i*16 + l%16 of stage wm, chunk
+                // (wn*16 + 2j + l/32) ^ (row % 32) = 16*(wn ^ (i%2)) +
+                // ((l/32 ^ l%16) ^ 2j), byte 8*((l/16) % 2) of it.
+                static_assert(T::kPasses == 1 && T::kRowsPerStage == WTM && WAVES_M == 2 && WAVES_N == 2 &&
+                              T::kLDC == 256 && T::kCCh == 32 && NT == 256 && NACC == 4,
+                              "the 256 x 256 four-wave tile");
+                const int lr = lane_e & 15, lh = (lane_e >> 4) & 1, lq = lane_e >> 5;
+                char* const sb = wm_e == 0 ? st0 : st1;
+                const uint32_t base_e = (uint32_t)(lr * 512 + lh * 8);
+                const uint32_t tx = (uint32_t)((lq ^ lr) << 4);
+                uint32_t o[2][NJ];
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j)
+                        o[q][j] = base_e + 256u * (uint32_t)(wn_e ^ q) + (tx ^ (uint32_t)(j << 5));
+                static_for<MI>([&](auto ic) __attribute__((always_inline)) {
+                    constexpr int i = decltype(ic)::value;
+                    static_for<NJ>([&](auto jc) __attribute__((always_inline)) {
+                        constexpr int j = decltype(jc)::value;
+                        u32x2_t v;
+                        v[0] = pack2<DT>(acc[i][j][0], acc[i][j][1]);
+                        v[1] = pack2<DT>(acc[i][j][2], acc[i][j][3]);
+                        *reinterpret_cast<u32x2_t*>(sb + o[i & 1][j] + i * 8192) = v;
+                    });
+                });
+            } else if (wm_e * WTM >= r0 && wm_e * WTM < r0 + T::kRowsPerPass) {
 #pragma unroll
                 for (int i = 0; i < MI; ++i) {
                     const int m = wm_e * WTM - r0 + i * MF + (lane_e & (MF - 1));
@@ -602,11 +652,28 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& a) {
                 constexpr int CPR = BN / 8;             // 16-byte chunks per tile row
                 constexpr int RPP = NT / CPR;           // rows per pass of the workgroup
                 const int c = tid_e % CPR;
+                if constexpr (MF == 16) {
+                    // thread t stores chunk c of tile rows r = t/32 + 8k
+                    // (k < 32): stage k/16, staging row r % 128, chunk
+                    // c ^ (r % 32) = c ^ (t/32 + 8 (k % 4))
+                    const int r0t = tid_e / CPR;
+                    uint32_t y[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) y[q] = (uint32_t)(((c ^ (r0t + 8 * q)) << 4) + r0t * 512);
+                    static_for<32>([&](auto kc) __attribute__((always_inline)) {
+                        constexpr int k = decltype(kc)::value;
+                        const char* sb = k < 16 ? st0 : st1;
+                        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(sb + y[k & 3] + 4096 * (k & 15));
+                        __builtin_amdgcn_raw_buffer_store_b128(v, rC, (uint32_t)((row_off[r0t + 8 * k] + c * 8) * 2),
+                                                               0, kCachePolicySc1);
+                    });
+                } else {
 #pragma unroll 4
-                for (int r = tid_e / CPR; r < T::kRowsPerPass; r += RPP) {
-                    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(cptr(r, c * 8));
-                    __builtin_amdgcn_raw_buffer_store_b128(v, rC, (uint32_t)((row_off[r0 + r] + c * 8) * 2), 0,
-                                                           kCachePolicySc1);
+                    for (int r = tid_e / CPR; r < T::kRowsPerPass; r += RPP) {
+                        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(cptr(r, c * 8));
+                        __builtin_amdgcn_raw_buffer_store_b128(v, rC, (uint32_t)((row_off[r0 + r] + c * 8) * 2), 0,
+                                                               kCachePolicySc1);
+                    }
                 }
             } else if (coherent) {
                 // Device-coherent 8-byte stores for outputs past a 31-bit
