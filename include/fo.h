@@ -490,8 +490,9 @@ void fo_get_sync_mode(int32_t* producer, int32_t* consumer);
 /* Grid of a consumer launch that runs beside the GEMM (every
  * fo_consume_group call, and every group but the last in fo_run_overlapped):
  * at most max_blocks workgroups (1 .. 256) of `threads` threads (64, 128 or
- * 256); default 256 x 256. A smaller grid streams a group more slowly and
- * spreads its memory traffic over more of the GEMM's run. Env
+ * 256); default 256 x 64, one wave per compute unit. A smaller grid streams
+ * a group more slowly and spreads its memory traffic over more of the GEMM's
+ * run. Env
  * FO_CONSUMER_BLOCKS / FO_CONSUMER_THREADS override at load time.
  * Process default of fo_options.consumer_blocks / consumer_threads;
  * FO_ERR_ARG outside the ranges. */

@@ -47,12 +47,14 @@ int env_int(const char* name, int lo, int hi, int dflt) {
     return dflt;
 }
 bool valid_threads(long t) { return t == 64 || t == 128 || t == 256; }
-// Grid of the consumers that run beside the GEMM (default: the full grid,
-// one 256-thread workgroup per compute unit).
+// Grid of the consumers that run beside the GEMM (default: one workgroup of
+// one wave per compute unit; beside the 256x256 GEMM, one wave per compute
+// unit costs the GEMM about half of what a wave on each SIMD costs, and the
+// group still streams well inside the compute of the groups after it).
 std::atomic<int> g_consumer_blocks{env_int("FO_CONSUMER_BLOCKS", 1, kMaxConsumeBlocks, kMaxConsumeBlocks)};
 std::atomic<int> g_consumer_threads{[] {
-    const int t = env_int("FO_CONSUMER_THREADS", 64, 256, 256);
-    return valid_threads(t) ? t : 256;
+    const int t = env_int("FO_CONSUMER_THREADS", 64, 256, 64);
+    return valid_threads(t) ? t : 64;
 }()};
 
 fo_options defaults() {
