@@ -173,14 +173,22 @@ def make_plan(w, inp, num_cus, sizes=None, pattern=None, gemm_us=0.0, curve=None
               row_bucket=bucket if pattern == "subtoken" else None, dest_bytes=DEST_BYTES)
     if sizes is not None:
         if curve is not None:      # given partition + Algorithm 1's estimate of it
-            return fo.plan_groups(w.M, w.N, w.K, sizes=list(sizes), gemm_us=gemm_us, curve_bytes=curve[0],
-                                  curve_us=curve[1], **kw)
+            return fo.plan_groups(w.M, w.N, w.K, sizes=list(sizes), gemm_us=gemm_us, **curve_kw(curve), **kw)
         return fo.plan_groups(w.M, w.N, w.K, sizes=list(sizes), **kw)
     if curve is None:
         tiles = (w.M // w.tile_m) * (w.N // w.tile_n)
         return fo.plan_groups(w.M, w.N, w.K, sizes=[-(-tiles // num_cus)], **kw)
-    return fo.plan_groups(w.M, w.N, w.K, sizes=None, gemm_us=gemm_us, curve_bytes=curve[0],
-                          curve_us=curve[1], s_first=2, s_last=4, **kw)
+    return fo.plan_groups(w.M, w.N, w.K, sizes=None, gemm_us=gemm_us, s_first=2, s_last=4, **curve_kw(curve),
+                          **kw)
+
+
+def curve_kw(curve):
+    """Planner keywords of a curve: (bytes, us) of the groups beside the
+    GEMM, optionally followed by (bytes, us) of the last group's."""
+    kw = dict(curve_bytes=curve[0], curve_us=curve[1])
+    if len(curve) > 2:
+        kw.update(last_curve_bytes=curve[2], last_curve_us=curve[3])
+    return kw
 
 
 def run_step(torch, w, plan, dp, b, s1, s2, ev=None):
@@ -241,21 +249,81 @@ def consume_all(torch, w, b, stream, n, iters, warmup):
                                                      opts=full), iters, warmup, stream)
 
 
-def consumer_curve(torch, w, b, stream, total_elems):
+def consumer_curve(torch, w, b, stream, total_elems, beside=None):
     """Consumer latency vs bytes (one launch, no wait, the grid the consumers
     beside the GEMM use): the 1-GPU stand-in for the communication bandwidth
-    curve the search interpolates."""
-    xs, ys = [], []
+    curve the search interpolates. With beside = (plan, dev_plan) each
+    launch is timed while that GEMM runs on another stream (every group but
+    the last streams beside the GEMM, and there the stand-in is slower than
+    alone); without, alone."""
+    sizes = []
     n = 1 << 15
     while n <= total_elems:
-        us = time_loop(torch, lambda: fo.consume_group(b.C, b.peer, b.dst, n, w.dtype, None, 0, None, stream,
-                                                       opts=OPTS), 20, 3, stream)
-        xs.append(2.0 * n)
-        ys.append(us)
+        sizes.append(n)
         if n == total_elems:
             break
         n = min(n * 2, total_elems)
-    return xs, ys
+    launch = lambda n: fo.consume_group(b.C, b.peer, b.dst, n, w.dtype, None, 0, None, stream, opts=OPTS)
+    if beside is None:
+        return [2.0 * n for n in sizes], [time_loop(torch, lambda: launch(n), 20, 3, stream) for n in sizes]
+    plan, dp = beside
+    sg = torch.cuda.Stream()
+    ys = []
+    for n in sizes:
+        vals = []
+        for r in range(6):
+            eg, e0, e1 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            eg.record(sg)
+            for _ in range(2):        # about 700 us of GEMM for the consumer to run beside
+                fo.gemm_signal_reorder(plan, dp, b.A, b.W, b.C, None, sg)
+            stream.wait_event(eg)
+            e0.record(stream)
+            launch(n)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            if r > 0:
+                vals.append(e0.elapsed_time(e1) * 1000.0)
+        ys.append(float(np.median(vals)))
+    return [2.0 * n for n in sizes], ys
+
+
+def consumer_curve_after(torch, w, b, inp, num_cus, s1, s2, total_elems):
+    """The last group's latency vs bytes: a consumer on the full grid, on the
+    communication stream, waiting for the GEMM's one group counter (a plan of
+    one group), timed from the GEMM's end to its own end -- the part of an
+    overlapped run that follows the GEMM."""
+    tiles = (w.M // w.tile_m) * (w.N // w.tile_n)
+    one = make_plan(w, inp, num_cus, sizes=[-(-tiles // num_cus)])
+    dp = dev_plan(torch, one)
+    full = fo.options(consumer_blocks=256, consumer_threads=256)
+    if OPTS is not None:
+        full.consumer_limit = OPTS.consumer_limit
+    sizes = []
+    n = 1 << 15
+    while n <= total_elems:
+        sizes.append(n)
+        if n == total_elems:
+            break
+        n = min(n * 2, total_elems)
+    ys = []
+    for n in sizes:
+        vals = []
+        for r in range(5):
+            er, eg, e1 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            fo.reset_counters(b.counters, one.num_counters, s1)
+            er.record(s1)
+            fo.gemm_signal_reorder(one, dp, b.A, b.W, b.C, b.counters, s1)
+            eg.record(s1)
+            s2.wait_event(er)
+            fo.consume_group(b.C, b.peer, b.dst, n, w.dtype, b.counters, int(one.targets[0]), b.status, s2,
+                             opts=full)
+            e1.record(s2)
+            torch.cuda.synchronize()
+            if r > 0:
+                vals.append(eg.elapsed_time(e1) * 1000.0)
+        ys.append(float(np.median(vals)))
+    check_status(b, "the last group's latency curve")
+    return [2.0 * n for n in sizes], ys
 
 
 def gemm_comm_times(torch, w, plan, dp, b, s1, s2, steps, with_gemm=False):
@@ -432,11 +500,12 @@ def workload_summary(torch, name, num_cus, steps):
     dp_base = dev_plan(torch, base_plan)
     torch.cuda.synchronize()
     sig_us = time_gemm(torch, base_plan, dp_base, b, s1, 30, 20)
-    xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N)
+    xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N, beside=(base_plan, dp_base))
+    lx, ly = consumer_curve_after(torch, w, b, inp, num_cus, s1, s2, w.M * w.N)
     if w.groups is not None:
         plan, dp = base_plan, dp_base
     else:
-        plan = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys))
+        plan = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys, lx, ly))
         dp = dev_plan(torch, plan)
     torch.cuda.synchronize()
     r = overlap_rounds(torch, w, plan, dp, base_plan, dp_base, b, s1, s2, 3, max(6, steps // 4))
@@ -469,7 +538,7 @@ def planner_report(w, inp, num_cus, gemm_us, curve):
     representative sizes of the same family (M/4, M/2, 2M; the GEMM time
     scaled with M), and the estimated latency of the cached partitions at
     unseen sizes against the search's own optimum there."""
-    xs, ys = curve
+    ckw = curve_kw(curve)
     kw = dict(dtype=w.dtype, tile_m=w.tile_m, tile_n=w.tile_n, order=w.order, num_cus=num_cus,
               pattern=w.pattern, num_dest=w.num_dest if w.pattern in ("subtile", "subtoken") else 0,
               dest_perm=inp.sigma if w.pattern == "subtile" else None, dest_bytes=DEST_BYTES)
@@ -480,7 +549,7 @@ def planner_report(w, inp, num_cus, gemm_us, curve):
 
     def search(M, b):
         return fo.plan_groups(M, w.N, w.K, row_bucket=b, sizes=None, gemm_us=gemm_us * M / w.M,
-                              curve_bytes=xs, curve_us=ys, s_first=2, s_last=4, **kw)
+                              s_first=2, s_last=4, **ckw, **kw)
 
     b = bucket(w.M)
     reps = 20
@@ -492,7 +561,7 @@ def planner_report(w, inp, num_cus, gemm_us, curve):
     reps_m = [m for m in (w.M // 4, w.M // 2, 2 * w.M) if m % w.tile_m == 0 and m > 0]
     for m in reps_m:
         cache.add(m, w.N, w.K, row_bucket=bucket(m), sizes=None, gemm_us=gemm_us * m / w.M,
-                  curve_bytes=xs, curve_us=ys, s_first=2, s_last=4, **kw)
+                  s_first=2, s_last=4, **ckw, **kw)
     t0 = time.perf_counter()
     for _ in range(reps):
         cache.lookup(w.M, w.N, w.K, row_bucket=b, **kw)
@@ -505,7 +574,7 @@ def planner_report(w, inp, num_cus, gemm_us, curve):
         bm = bucket(m)
         plan, matched = cache.lookup(m, w.N, w.K, row_bucket=bm, **kw)
         est = fo.plan_groups(m, w.N, w.K, row_bucket=bm, sizes=list(plan.sizes), gemm_us=gemm_us * m / w.M,
-                             curve_bytes=xs, curve_us=ys, **kw).predicted_us
+                             **ckw, **kw).predicted_us
         best = search(m, bm)
         unseen.append({"M": m, "matched_M": matched, "cached_groups": [int(x) for x in plan.sizes],
                        "searched_groups": [int(x) for x in best.sizes],
@@ -534,13 +603,14 @@ def predictor_accuracy(torch, w, inp, b, base_plan, dp_base, num_cus, T, flops, 
     measured time against the best measured one."""
     log("predictor: GEMM alone and consumer curve")
     sig_us = time_gemm(torch, base_plan, dp_base, b, s1, 50, 10)
-    xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N)
+    xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N, beside=(base_plan, dp_base))
+    lx, ly = consumer_curve_after(torch, w, b, inp, num_cus, s1, s2, w.M * w.N)
     cands = partitions(T)
     plans = {}
     for c in cands:
-        p = make_plan(w, inp, num_cus, sizes=c, gemm_us=sig_us, curve=(xs, ys))
+        p = make_plan(w, inp, num_cus, sizes=c, gemm_us=sig_us, curve=(xs, ys, lx, ly))
         plans[c] = (p, dev_plan(torch, p))
-    searched = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys))
+    searched = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys, lx, ly))
     torch.cuda.synchronize()
     meas = {c: [] for c in cands}
     gemm_in = []
@@ -560,7 +630,7 @@ def predictor_accuracy(torch, w, inp, b, base_plan, dp_base, num_cus, T, flops, 
     for c in cands:
         m = float(np.median(meas[c]))
         pr = plans[c][0].predicted_us
-        pr_ov = make_plan(w, inp, num_cus, sizes=c, gemm_us=gemm_ov, curve=(xs, ys)).predicted_us
+        pr_ov = make_plan(w, inp, num_cus, sizes=c, gemm_us=gemm_ov, curve=(xs, ys, lx, ly)).predicted_us
         rows.append({"groups": list(c), "predicted_us": round(pr, 2), "measured_us": round(m, 2),
                      "error_pct": round((pr - m) / m * 100, 2),
                      "predicted_overlap_gemm_us": round(pr_ov, 2),
@@ -684,8 +754,9 @@ def slow_link(torch, w, inp, b, base_plan, dp_base, num_cus, s1, s2):
     try:
         for cap in (0, 64, 32, 16, 8):
             OPTS = fo.options(consumer_limit=cap)
-            xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N)
-            p = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys))
+            xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N, beside=(base_plan, dp_base))
+            lx, ly = consumer_curve_after(torch, w, b, inp, num_cus, s1, s2, w.M * w.N)
+            p = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys, lx, ly))
             d = dev_plan(torch, p)
             torch.cuda.synchronize()
             ov, se = [], []
@@ -693,7 +764,7 @@ def slow_link(torch, w, inp, b, base_plan, dp_base, num_cus, s1, s2):
                 ov.append(timed_steps(torch, w, p, d, b, s1, s2, 6, 2)[0])
                 se.append(timed_steps(torch, w, p, d, b, s1, s1, 6, 2)[0])
             o, r = float(np.median(ov)), float(np.median(se))
-            rows.append({"consumer_limit": cap, "consume_alone_us": round(ys[-1], 2),
+            rows.append({"consumer_limit": cap, "consume_beside_gemm_us": round(ys[-1], 2),
                          "consume_over_gemm": round(ys[-1] / sig_us, 3),
                          "groups": [int(x) for x in p.sizes], "predicted_us": round(p.predicted_us, 2),
                          "overlapped_step_us": round(o, 2), "serial_step_us": round(r, 2),
@@ -708,8 +779,9 @@ def sync_modes(torch, w, inp, b, base_plan, dp_base, num_cus, s1, s2):
     modes), the GEMM alone and the overlapped step with each."""
     global OPTS
     sig_us = time_gemm(torch, base_plan, dp_base, b, s1, 30, 5)
-    xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N)
-    plan = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys))
+    xs, ys = consumer_curve(torch, w, b, s1, w.M * w.N, beside=(base_plan, dp_base))
+    lx, ly = consumer_curve_after(torch, w, b, inp, num_cus, s1, s2, w.M * w.N)
+    plan = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys, lx, ly))
     dp = dev_plan(torch, plan)
     torch.cuda.synchronize()
     rows = {}
@@ -841,7 +913,8 @@ def main():
     plain_static_us, plain_sig_us, sig_us = (float(np.median(v)) for v in (plain_static, plain_sig, sig))
     log("consumer curve")
     n_all = w.M * w.N
-    xs, ys = consumer_curve(torch, w, b, s1, n_all)
+    xs, ys = consumer_curve(torch, w, b, s1, n_all, beside=(base_plan, dp_base))
+    lx, ly = consumer_curve_after(torch, w, b, inp, num_cus, s1, s2, n_all)
     cons_bytes_per_elem = 6 if b.peer is not None else 4
     cons_all_us = consume_all(torch, w, b, s1, n_all, 20, 3)
 
@@ -849,11 +922,11 @@ def main():
     if args.sizes:
         plan = make_plan(w, inp, num_cus, sizes=[int(x) for x in args.sizes.split(",")])
     else:
-        plan = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys))
+        plan = make_plan(w, inp, num_cus, gemm_us=sig_us, curve=(xs, ys, lx, ly))
     dp = dev_plan(torch, plan)
     torch.cuda.synchronize()
     log(f"plan: T={plan.T} groups={list(plan.sizes)} predicted {plan.predicted_us:.1f} us")
-    planner = planner_report(w, inp, num_cus, sig_us, (xs, ys)) if not args.sizes else None
+    planner = planner_report(w, inp, num_cus, sig_us, (xs, ys, lx, ly)) if not args.sizes else None
 
     # ---- overlapped vs serialized, alternating rounds ----------------------
     log("overlapped vs serialized rounds")
@@ -966,7 +1039,8 @@ def main():
         "consumer": {"whole_buffer_us": round(cons_all_us, 2),
                      "GBps": round(cons_bytes_per_elem * n_all / cons_all_us / 1e3, 1),
                      "frac_hbm": round(cons_bytes_per_elem * n_all / cons_all_us / 1e3 / PEAK_HBM_GBS, 4),
-                     "whole_buffer_beside_gemm_grid_us": round(ys[-1], 2),
+                     "whole_buffer_beside_running_gemm_us": round(ys[-1], 2),
+                     "whole_buffer_after_gemm_us": round(ly[-1], 2),
                      "beside_gemm_grid": "%dx%d" % fo.get_consumer_grid()},
         "post_reorder": {"us": round(post_us, 2), "identity_map_us": round(post_id_us, 2),
                          "GBps": round(post_bytes / post_us / 1e3, 1),

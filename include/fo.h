@@ -124,6 +124,13 @@ typedef struct {
                                  across GPUs); 1 = all its pieces (one device moves
                                  every piece, as the one-GPU stand-in consumer
                                  does). Other patterns ignore it.                  */
+    const double* last_curve_bytes; /* optional latency curve of the LAST group's */
+    const double* last_curve_us;    /*   communication, which runs after the GEMM */
+    int32_t last_curve_len;         /*   has ended: same form as `curve`; 0 = the
+                                         last group uses `curve` too. (A one-GPU
+                                         stand-in of the communication shares the
+                                         device with the GEMM until the last group
+                                         and has it to itself for that one.)       */
 } fo_grouping;
 
 typedef struct fo_plan fo_plan;   /* opaque, library-owned host memory */

@@ -455,16 +455,23 @@ def slot_range_bytes(plan: Plan, f0: int, f1: int, elem_bytes: int = 2, all_dest
 
 
 def search_partition(plan: Plan, gemm_us: float, curve_bytes, curve_us,
-                     s_first: int = 2, s_last: int = 4, elem_bytes: int = 2, all_dest: bool = False):
+                     s_first: int = 2, s_last: int = 4, elem_bytes: int = 2, all_dest: bool = False,
+                     last_curve=None):
     """Algorithm 1 on a plan's geometry (its waves, tiles and pools; its own
-    partition is ignored). Returns (partition in waves, predicted us)."""
+    partition is ignored). Returns (partition in waves, predicted us).
+    ``last_curve`` = (bytes, us): the latency curve of the last group's
+    communication, which runs once the GEMM is over; None: the one curve for
+    every group. (The paper has one curve; a second one for the last group
+    is this implementation's reading for a one-GPU stand-in of the
+    communication, which shares the device with the GEMM until then.)"""
     T = plan.T
 
     def comm_for(sizes):
         first = group_first_slots(sizes, "waves", plan.W, plan.tiles)
-        lat = [interp_latency(curve_bytes, curve_us,
-                              slot_range_bytes(plan, first[j], first[j + 1], elem_bytes, all_dest))
-               for j in range(len(sizes))]
+        lat = []
+        for j in range(len(sizes)):
+            xs, ys = (curve_bytes, curve_us) if last_curve is None or j < len(sizes) - 1 else last_curve
+            lat.append(interp_latency(xs, ys, slot_range_bytes(plan, first[j], first[j + 1], elem_bytes, all_dest)))
         return lambda j: lat[j]
 
     return predictive_search(T, gemm_us, comm_for, s_first, s_last)

@@ -64,7 +64,9 @@ class _Grouping(ctypes.Structure):
                 ("curve_bytes", ctypes.POINTER(ctypes.c_double)),
                 ("curve_us", ctypes.POINTER(ctypes.c_double)), ("curve_len", ctypes.c_int32),
                 ("s_first", ctypes.c_int32), ("s_last", ctypes.c_int32),
-                ("all_dest_bytes", ctypes.c_int32)]
+                ("all_dest_bytes", ctypes.c_int32),
+                ("last_curve_bytes", ctypes.POINTER(ctypes.c_double)),
+                ("last_curve_us", ctypes.POINTER(ctypes.c_double)), ("last_curve_len", ctypes.c_int32)]
 
 
 class _Options(ctypes.Structure):
@@ -304,18 +306,23 @@ _DEST_BYTES = {"largest": 0, "all": 1}
 
 
 def _grouping(sizes: Optional[Sequence[int]] = None, unit="waves", gemm_us: float = 0.0,
-              curve_bytes=None, curve_us=None, s_first: int = 2, s_last: int = 4, dest_bytes: str = "largest"):
+              curve_bytes=None, curve_us=None, s_first: int = 2, s_last: int = 4, dest_bytes: str = "largest",
+              last_curve_bytes=None, last_curve_us=None):
     """An fo_grouping and the arrays it points to."""
     sz = _i32_array(sizes)
     cb, cu = _f64_array(curve_bytes), _f64_array(curve_us)
+    lb, lu = _f64_array(last_curve_bytes), _f64_array(last_curve_us)
     grp = _Grouping(unit=_UNITS[unit], num_groups=0 if sizes is None else len(sizes),
                     sizes=ctypes.cast(sz, ctypes.POINTER(ctypes.c_int32)) if sz is not None else None,
                     gemm_us=gemm_us,
                     curve_bytes=ctypes.cast(cb, ctypes.POINTER(ctypes.c_double)) if cb is not None else None,
                     curve_us=ctypes.cast(cu, ctypes.POINTER(ctypes.c_double)) if cu is not None else None,
                     curve_len=0 if curve_bytes is None else len(curve_bytes),
-                    s_first=s_first, s_last=s_last, all_dest_bytes=_DEST_BYTES[dest_bytes])
-    return grp, (sz, cb, cu)
+                    s_first=s_first, s_last=s_last, all_dest_bytes=_DEST_BYTES[dest_bytes],
+                    last_curve_bytes=ctypes.cast(lb, ctypes.POINTER(ctypes.c_double)) if lb is not None else None,
+                    last_curve_us=ctypes.cast(lu, ctypes.POINTER(ctypes.c_double)) if lu is not None else None,
+                    last_curve_len=0 if last_curve_bytes is None else len(last_curve_bytes))
+    return grp, (sz, cb, cu, lb, lu)
 
 
 _PROBLEM_KEYS = ("dtype", "tile_m", "tile_n", "order", "group_m", "num_xcds", "num_cus", "wg_per_cu",
@@ -338,8 +345,9 @@ def plan_groups(M: int, N: int, K: int, **kw) -> Plan:
     order, group_m, num_xcds, num_cus, wg_per_cu, reserved_cus, pattern,
     num_dest, dest_perm, row_bucket) and the fo_grouping ones (sizes, unit,
     gemm_us, curve_bytes, curve_us, s_first, s_last, dest_bytes = "largest" or
-    "all": an All-to-All group's data size in the estimate); sizes=None runs
-    the Algorithm 1 search (needs gemm_us and the latency curve)."""
+    "all": an All-to-All group's data size in the estimate, last_curve_bytes /
+    last_curve_us: the last group's latency curve); sizes=None runs the
+    Algorithm 1 search (needs gemm_us and the latency curve)."""
     L = lib()
     prob_kw, grp_kw = _split(kw)
     prob, keep_p = _problem(M, N, K, **prob_kw)

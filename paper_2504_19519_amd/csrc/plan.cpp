@@ -66,13 +66,17 @@ double range_bytes(const fo_plan& p, int32_t f0, int32_t f1, bool all_dest) {
 // up to and including g; its communication starts once that computation and
 // the previous group's communication are both done, and takes the curve's
 // latency for the group's bytes: E_g = max(C_g, E_(g-1)) + comm(g), with
-// E_(-1) = 0. The partition's latency is the last group's E.
+// E_(-1) = 0. The partition's latency is the last group's E. The last
+// group's latency comes from the grouping's second curve when it has one
+// (its communication runs after the GEMM).
 double predict(const fo_plan& p, const std::vector<int32_t>& sizes, double gemm_us,
                const fo_grouping& g, std::vector<int32_t>& first_scratch) {
     firsts_from_waves(sizes, p.W, p.tiles, first_scratch);
     auto comm = [&](size_t j) {
-        return interp_latency(g.curve_bytes, g.curve_us, g.curve_len,
-                              range_bytes(p, first_scratch[j], first_scratch[j + 1], g.all_dest_bytes != 0));
+        const double bytes = range_bytes(p, first_scratch[j], first_scratch[j + 1], g.all_dest_bytes != 0);
+        if (j + 1 == sizes.size() && g.last_curve_len > 0)
+            return interp_latency(g.last_curve_bytes, g.last_curve_us, g.last_curve_len, bytes);
+        return interp_latency(g.curve_bytes, g.curve_us, g.curve_len, bytes);
     };
     double compute_done = 0.0;   // C_g
     double comm_done = 0.0;      // E_(g-1), then E_g
@@ -88,6 +92,13 @@ fo_status check_curve(const fo_grouping& g) {
         if (!(g.curve_bytes[i] > 0.0) || !(g.curve_us[i] >= 0.0) ||
             (i > 0 && !(g.curve_bytes[i] > g.curve_bytes[i - 1])))
             return fo::fail(FO_ERR_ARG, "curve bytes must be positive and ascending, latencies >= 0");
+    }
+    if (g.last_curve_len < 0 || (g.last_curve_len > 0 && (!g.last_curve_bytes || !g.last_curve_us)))
+        return fo::fail(FO_ERR_ARG, "last-group curve: length >= 0 and both arrays when it is > 0");
+    for (int i = 0; i < g.last_curve_len; ++i) {
+        if (!(g.last_curve_bytes[i] > 0.0) || !(g.last_curve_us[i] >= 0.0) ||
+            (i > 0 && !(g.last_curve_bytes[i] > g.last_curve_bytes[i - 1])))
+            return fo::fail(FO_ERR_ARG, "last-group curve bytes must be positive and ascending, latencies >= 0");
     }
     if (!(g.gemm_us >= 0.0)) return fo::fail(FO_ERR_ARG, "gemm_us must be >= 0");
     if (g.all_dest_bytes != 0 && g.all_dest_bytes != 1) return fo::fail(FO_ERR_ARG, "all_dest_bytes must be 0 or 1");

@@ -186,6 +186,23 @@ def test_alg1_closed_form_linear_comm():
     assert best == (1, 1) and t == pytest.approx(3.0)
 
 
+def test_alg1_last_group_curve_closed_form():
+    # T = 2, GEMM 2 us. Groups before the last: 2 us per wave of bytes; the
+    # last group (after the GEMM): 0.5 us per wave. (1,1) -> wave 1's
+    # communication 1..3, wave 2's 3..3.5: 3.5 us; (2) -> 2 + 2 * 0.5 = 3 us.
+    # With the slow curve for both, (1,1) -> 5 us beats (2) -> 6 us.
+    W, BM, BN = 4, 8, 8
+    wave_bytes = W * BM * BN * 2
+    plan = oracle.make_plan(2 * BM, 4 * BN, BM, BN, num_cus=W, sizes=(2,))
+    slow, fast = ([wave_bytes], [2.0]), ([wave_bytes], [0.5])
+    best, t = oracle.search_partition(plan, 2.0, *slow, last_curve=fast)
+    assert best == (2,) and t == pytest.approx(3.0)
+    best, t = oracle.search_partition(plan, 2.0, *slow)
+    assert best == (1, 1) and t == pytest.approx(5.0)
+    # the same curve given as the last group's changes nothing
+    assert oracle.search_partition(plan, 2.0, *slow, last_curve=slow) == (best, t)
+
+
 def test_alg1_closed_form_fixed_cost():
     # fixed 2 us per call plus 1 us per wave: (1,1) -> 7 us, (2) -> 6 us
     comm = lambda sizes: (lambda j: 2.0 + sizes[j])

@@ -125,6 +125,43 @@ def test_predictive_search_matches_oracle(seed, pattern, nd, dest_bytes):
     assert p.predicted_us == pytest.approx(t, rel=1e-12)
 
 
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("pattern,nd", [("tile", 0), ("subtoken", 8), ("subtile", 4)])
+def test_search_and_estimate_with_last_group_curve_match_oracle(seed, pattern, nd):
+    # a second curve for the last group (its communication after the GEMM):
+    # the search and the estimate of a given partition against the oracle
+    rng = np.random.default_rng(300 + seed)
+    M, N, BM, BN = 4096, 7168, 256, 128
+    cus = int(rng.choice([64, 128, 256]))
+    xs, ys = _curve(seed + 20)
+    lx, ly = _curve(seed + 40)
+    gemm_us = float(rng.uniform(20, 400))
+    bucket = rng.integers(0, nd, M) if pattern == "subtoken" else None
+    sigma = rng.permutation(nd) if pattern == "subtile" else None
+    kw = dict(num_cus=cus, pattern=pattern, num_dest=nd, row_bucket=bucket, dest_perm=sigma, gemm_us=gemm_us,
+              curve_bytes=xs, curve_us=ys, last_curve_bytes=lx, last_curve_us=ly)
+    p = fo.plan_groups(M, N, 2048, sizes=None, s_first=2, s_last=4, **kw)
+    o = oracle.make_plan(M, N, BM, BN, num_cus=cus, order="xcd", pattern=pattern, num_dest=nd,
+                         bucket=bucket, sigma=sigma, sizes=(-(-896 // cus),))
+    best, t = oracle.search_partition(o, gemm_us, xs, ys, 2, 4, last_curve=(lx, ly))
+    assert tuple(p.sizes) == best
+    assert p.predicted_us == pytest.approx(t, rel=1e-12)
+    T = -(-896 // cus)
+    cuts = sorted(rng.choice(np.arange(1, T), size=int(rng.integers(0, T)), replace=False)) if T > 1 else []
+    sizes = tuple(int(b - a) for a, b in zip([0] + list(cuts), list(cuts) + [T]))
+    q = fo.plan_groups(M, N, 2048, sizes=list(sizes), **kw)
+    first = oracle.group_first_slots(sizes, "waves", o.W, o.tiles)
+    lat = [oracle.interp_latency(*((lx, ly) if j == len(sizes) - 1 else (xs, ys)),
+                                 oracle.slot_range_bytes(o, first[j], first[j + 1], 2)) for j in range(len(sizes))]
+    assert q.predicted_us == pytest.approx(oracle.predicted_latency(sizes, T, gemm_us, lambda j: lat[j]), rel=1e-12)
+
+
+def test_last_group_curve_is_checked():
+    with pytest.raises(fo.FoError):
+        fo.plan_groups(4096, 7168, 2048, sizes=None, gemm_us=100.0, curve_bytes=[1e6, 1e8], curve_us=[5.0, 20.0],
+                       last_curve_bytes=[1e8, 1e6], last_curve_us=[5.0, 20.0])
+
+
 def test_search_single_wave_gives_one_group():
     # 2048 x 4096 in 256x128 tiles is 256 tiles: one wave on 256 CUs
     p = fo.plan_groups(2048, 4096, 4096, num_cus=256, sizes=None, gemm_us=40.0,
