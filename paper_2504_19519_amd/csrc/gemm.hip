@@ -12,17 +12,16 @@
 // conflict-free 16-byte fragment reads); fragments of the next MFMA k step are
 // read while the MFMAs of the current one run, and every LDS read and load
 // issue sits in the shadow of an MFMA. Two forms:
-//   256x256 tiles: 4 waves of 128 x 128 (one per SIMD), v_mfma_f32_16x16x32
-//     in inline asm with the accumulators tied in place (mostly AGPRs), two
-//     stages; a wave reads 2/3 of the LDS bytes per flop that 8 waves of
-//     128 x 64 read, which lets the power-limited clock run higher. A
-//     substep's 64 MFMAs carry the 16 fragment reads of the next substep and,
-//     after the step's barrier, the 16 load issues of the stage just freed,
-//     one every 4 MFMAs (bunched issues stall the single wave of a SIMD on
-//     the memory pipeline).
-//   256x128 and 64x64 tiles: 8 (or 4) waves of 64 x 64 (32 x 32),
-//     v_mfma_f32_32x32x16 from the compiler's builtin, loads issued STAGES
-//     steps ahead.
+//   256x256 and 256x128 tiles: 4 waves of 128 x 128 (128 x 64), one per
+//     SIMD, v_mfma_f32_16x16x32 in inline asm with the accumulators tied in
+//     place, two stages; a wave of 128 x 128 reads 2/3 of the LDS bytes per
+//     flop that 8 waves of 128 x 64 read, which lets the power-limited clock
+//     run higher. A substep's MFMAs carry the fragment reads of the next
+//     substep and, after the step's barrier, the load issues of the stage
+//     just freed, one every 4 (256x128: 2) MFMAs (bunched issues stall the
+//     single wave of a SIMD on the memory pipeline).
+//   64x64 tiles: 4 waves of 32 x 32, v_mfma_f32_32x32x16 from the compiler's
+//     builtin, loads issued STAGES steps ahead.
 // The main loop is the same for every output pattern (Section 5: only the
 // epilogue changes).
 //
@@ -398,8 +397,8 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& a) {
         const bool live = lkt < KT;
         const uint32_t ab = live ? (uint32_t)(BM * K * 2) : 0u, wb = live ? (uint32_t)(BN * K * 2) : 0u;
         const uint32_t so = live ? (uint32_t)lkt * (kBK * 2) : 0u;
-        constexpr int kGap = 4;
-        static_assert(MI * NJ >= kGap * T::kLoads, "a load issue every 4 MFMAs");
+        constexpr int kGap = (MI * NJ) / T::kLoads >= 4 ? 4 : (MI * NJ) / T::kLoads;
+        static_assert(kGap >= 1, "a load issue at least every MFMA");
         static_for<MI * NJ>([&](auto mc) __attribute__((always_inline)) {
             constexpr int m = decltype(mc)::value;
             constexpr int i = m / NJ, j = m % NJ;
@@ -594,7 +593,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& a) {
         for (int pass = 0; pass < T::kPasses; ++pass) {
             const int r0 = pass * T::kRowsPerPass;
             // accumulators of the waves whose rows are in this pass -> staging
-            if constexpr (MF == 16) {
+            if constexpr (MF == 16 && BN == 256) {
                 // 256 x 256 tile, 4 waves of 128 x 128, one pass: the
                 // addresses of cptr in closed form. Lane l of block (i, j)
                 // holds tile row wm*128 + i*16 + l%16, columns wn*128 + j*16 +
@@ -652,7 +651,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& a) {
                 constexpr int CPR = BN / 8;             // 16-byte chunks per tile row
                 constexpr int RPP = NT / CPR;           // rows per pass of the workgroup
                 const int c = tid_e % CPR;
-                if constexpr (MF == 16) {
+                if constexpr (MF == 16 && BN == 256) {
                     // thread t stores chunk c of tile rows r = t/32 + 8k
                     // (k < 32): stage k/16, staging row r % 128, chunk
                     // c ^ (r % 32) = c ^ (t/32 + 8 (k % 4))
@@ -783,6 +782,13 @@ __global__ __launch_bounds__(256, 1) __attribute__((amdgpu_num_vgpr(216))) void 
     gemm_body<DT, 256, 256, 2, 2, 2, 64, 16>(a);
 }
 
+// 256x128 tiles, 4 waves of 128x64 (16x16x32 MFMAs; 128 accumulator
+// registers per lane, no register cap needed).
+template <int DT>
+__global__ __launch_bounds__(256, 1) void gemm_w4n_kernel(const GemmArgs a) {
+    gemm_body<DT, 256, 128, 2, 2, 2, 64, 16>(a);
+}
+
 template <int DT, int BM, int BN, int WM, int WN, int ST, int BK>
 hipError_t launch_t(const GemmArgs& a, int grid, hipStream_t s) {
     hipLaunchKernelGGL((gemm_signal_kernel<DT, BM, BN, WM, WN, ST, BK>), dim3(grid), dim3(64 * WM * WN), 0, s, a);
@@ -798,9 +804,11 @@ hipError_t launch_w4(const GemmArgs& a, int grid, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_gemm(int dtype, int tile_m, int tile_n, const GemmArgs& a, int grid, hipStream_t s) {
-    if (tile_m == 256 && tile_n == 128)
-        return dtype == FO_FP16 ? launch_t<FO_FP16, 256, 128, 4, 2, 3, 64>(a, grid, s)
-                                : launch_t<FO_BF16, 256, 128, 4, 2, 3, 64>(a, grid, s);
+    if (tile_m == 256 && tile_n == 128) {
+        if (dtype == FO_FP16) hipLaunchKernelGGL(gemm_w4n_kernel<FO_FP16>, dim3(grid), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL(gemm_w4n_kernel<FO_BF16>, dim3(grid), dim3(256), 0, s, a);
+        return hipGetLastError();
+    }
     if (tile_m == 256 && tile_n == 256)
         return dtype == FO_FP16 ? launch_w4<FO_FP16>(a, grid, s) : launch_w4<FO_BF16>(a, grid, s);
     if (tile_m == 64 && tile_n == 64)

@@ -36,7 +36,8 @@ def _regs(v):
 
 def test_consumer_fits_beside_every_gemm_kernel():
     u = _usage()
-    gemm = {k: v for k, v in u.items() if "gemm_signal_kernel" in k or "gemm_w4_kernel" in k}
+    gemm = {k: v for k, v in u.items()
+            if "gemm_signal_kernel" in k or "gemm_w4_kernel" in k or "gemm_w4n_kernel" in k}
     cons = {k: v for k, v in u.items() if "consume_kernel" in k}
     assert len(gemm) >= 6 and len(cons) >= 8
     c_regs = max(_regs(v) for v in cons.values())
@@ -44,8 +45,8 @@ def test_consumer_fits_beside_every_gemm_kernel():
     for name, v in gemm.items():
         # register spills may only go to other registers (no scratch memory)
         assert v.get("scratch", 0) == 0, name
-        if "gemm_w4_kernel" in name:
-            per_simd = 1                   # 4 waves of 128 x 128: one per SIMD
+        if "gemm_w4_kernel" in name or "gemm_w4n_kernel" in name:
+            per_simd = 1                   # 4 waves of 128 x 128 (128 x 64): one per SIMD
         else:
             # waves of one GEMM workgroup per SIMD (template arguments: dtype,
             # tile_m, tile_n, waves_m, waves_n, stages, k step): 4 waves -> 1, 8 -> 2
