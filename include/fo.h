@@ -415,8 +415,8 @@ fo_status fo_reset_counters(uint32_t* counters, int32_t n, void* stream);
  * With comm_stream == gemm_stream (or NULL) the same work runs serialized
  * on gemm_stream, without the handoffs and without signalling. A plan of one
  * group has nothing to overlap (its consumer can only start after the whole
- * GEMM): with a comm_stream it runs serialized on gemm_stream too, but the
- * GEMM still signals the counters. An overlapped run needs counters and,
+ * GEMM): with a comm_stream it runs serialized on gemm_stream too, the same
+ * way (counters untouched). An overlapped run needs counters and,
  * with more than one group, a created gemm_stream (not the null stream,
  * which would wait for the gate kernel on a blocking comm_stream).
  * Buffers: C_out (GEMM output, see fo_gemm_signal_reorder), peer (NULL for

@@ -445,7 +445,7 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
     if (!dst) return fo::fail(FO_ERR_ARG, "dst is NULL");
     // An overlapped run with one group has nothing to overlap (its consumer
     // can only start once the whole GEMM is done): it runs on the GEMM stream
-    // alone, still signalling, without the stream handoffs.
+    // alone, as a serialized run does (no handoffs, no signalling).
     const bool requested = comm_stream && comm_stream != gemm_stream;
     const bool overlap = requested && plan->P > 1;
     if (requested && !counters) return fo::fail(FO_ERR_ARG, "an overlapped run needs counters");
@@ -466,7 +466,7 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
     const uint32_t seq = fo::g_run_seq.fetch_add(1, std::memory_order_relaxed);
     const uint32_t tag = fo::kGateTag | (seq & fo::kGateSeqMask);
     const uint32_t done_tag = fo::done_tag_of(seq);
-    if (requested) {
+    if (overlap) {
         hipLaunchKernelGGL(fo::reset_run_kernel, dim3(1), dim3(256), 0, s1, counters, plan->P + FO_DISPENSER_WORDS,
                            done, done_tag, status_word, gate, tag);
         if ((e = hipGetLastError()) != hipSuccess) return fo::hip_fail("reset kernel launch", e);
@@ -475,7 +475,7 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
         return fo::hip_fail("gate kernel launch", e);
     if (gemm_begin_event && (e = hipEventRecord((hipEvent_t)gemm_begin_event, s1)) != hipSuccess)
         return fo::hip_fail("hipEventRecord", e);
-    if ((st = fo_gemm_signal_reorder(plan, dev_plan, A, W, C_out, requested ? counters : nullptr, s1, &o)) !=
+    if ((st = fo_gemm_signal_reorder(plan, dev_plan, A, W, C_out, overlap ? counters : nullptr, s1, &o)) !=
         FO_OK)
         return st;
     if (gemm_end_event && (e = hipEventRecord((hipEvent_t)gemm_end_event, s1)) != hipSuccess)

@@ -93,7 +93,8 @@ def check(w, inp, plan, o, sample_rows=None, opts=None):
         assert_close_bits(C_plain.reshape(w.M, w.N)[rows], ref, w.dtype, "GEMM (sampled rows)")
     Cr, dst, out, counters, status = run(w, plan, d, overlap=True)
     assert status == 0
-    np.testing.assert_array_equal(counters, np.array(o.targets))
+    # a plan of one group runs serialized and leaves the counters alone
+    np.testing.assert_array_equal(counters, np.array(o.targets) if plan.P > 1 else np.zeros(plan.P, np.int64))
     np.testing.assert_array_equal(Cr, C_plain[oracle.reorder_index(o)])
     dst_ref = oracle.apply_consumer(o, Cr, inp.peer if w.pattern != "subtoken" else None, w.dtype)
     np.testing.assert_array_equal(dst, dst_ref)
