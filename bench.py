@@ -94,7 +94,7 @@ class Bufs:
         self.C = torch.empty(n, dtype=torch.int16, device=dev)
         self.dst = torch.empty(max(dest_elems, n), dtype=torch.int16, device=dev)
         self.out = torch.empty(n, dtype=torch.int16, device=dev)
-        self.counters = torch.zeros(64, dtype=torch.int32, device=dev)
+        self.counters = torch.zeros(1024, dtype=torch.int32, device=dev)   # >= fo_plan_num_counters of any plan here
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
 
 

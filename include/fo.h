@@ -198,9 +198,10 @@ int32_t fo_plan_num_groups(const fo_plan* plan);      /* P                      
 /* Length of the counters array of a signalling run: P group counters, then
  * FO_DISPENSER_WORDS tile-position counters of the GEMM, then
  * FO_HANDOFF_WORDS words that fo_run_overlapped uses to hand work between
- * its two streams. */
+ * its two streams (a gate word, then 8 done words 32 words apart, each in a
+ * 128-byte line of its own). */
 #define FO_DISPENSER_WORDS 8
-#define FO_HANDOFF_WORDS 2
+#define FO_HANDOFF_WORDS 226
 int32_t fo_plan_num_counters(const fo_plan* plan);    /* P + FO_DISPENSER_WORDS
                                                          + FO_HANDOFF_WORDS       */
 const int32_t* fo_plan_group_sizes(const fo_plan* plan);   /* [P], in the plan's unit */
@@ -389,13 +390,15 @@ fo_status fo_reset_counters(uint32_t* counters, int32_t n, void* stream);
  *   comm_stream: gate kernel -> one consumer launch per group
  * The two streams hand work to each other on the device, not with events:
  * the reset kernel zeroes counters[0, P + FO_DISPENSER_WORDS), writes the
- * run's tag (a process-wide sequence number) into the done word
- * counters[P + FO_DISPENSER_WORDS + 1] with a count of zero, then writes the
- * tag into the gate word counters[P + FO_DISPENSER_WORDS]; the gate kernel
- * (one wave) holds the consumers until it reads that tag; each workgroup of
- * the final consumer launch adds 1 to the done word only while the word
- * carries its own run's tag, and the done wait (one wave) holds the
- * post-reorder until the count reaches the launch's grid. A consumer of an
+ * run's tag (a process-wide sequence number) into the 8 done words
+ * counters[P + FO_DISPENSER_WORDS + 1 + 32 k] with a count of zero, then
+ * writes the tag into the gate word counters[P + FO_DISPENSER_WORDS]; the
+ * gate kernel (one wave) holds the consumers until it reads that tag;
+ * workgroup b of the final consumer launch adds 1 to done word b % 8 only
+ * while that word carries its own run's tag, and the done wait (one wave)
+ * holds the post-reorder until every done word has counted its share of the
+ * launch's grid (spreading the count keeps the workgroups' adds from queueing
+ * on one address). A consumer of an
  * earlier run that finishes late therefore does not count for a later run
  * (it can only race with the later run's reset, the check and the add being
  * two steps, if a wait of the earlier run timed out: then the status bit is

@@ -25,8 +25,9 @@ struct ConsumeArgs {
     uint32_t target;
     uint32_t* status;            // bit 0 set on a timed-out wait (may be nullptr)
     uint64_t timeout_ticks;      // wall-clock ticks
-    uint32_t* done;              // non-null: each workgroup adds 1 when its stores are visible,
-                                 // while the word's high half equals done_tag's
+    uint32_t* done;              // non-null: done word 0; workgroup b adds 1 to word b % kDoneWords
+                                 // (kDoneStride words apart) when its stores are visible, while
+                                 // that word's high half equals done_tag's
     uint32_t done_tag;           // run tag of the done word (done_tag_of)
     int32_t nseg;                // 1 .. kMaxConsumeSegments
     ConsumeSegment seg[kMaxConsumeSegments];
@@ -56,10 +57,23 @@ hipError_t launch_wait(const uint32_t* counter, uint32_t target, uint32_t* statu
 constexpr uint32_t kGateTag = 0x80000000u;
 constexpr uint32_t kGateTimedOut = 0x40000000u;
 constexpr uint32_t kGateSeqMask = kGateTimedOut - 1;
-// Done word of an overlapped run: the low 16 bits of the run's sequence
-// number in the high half, the count of finished final-consumer workgroups
-// (at most kMaxConsumeBlocks) in the low half.
+// Done words of an overlapped run: the low 16 bits of the run's sequence
+// number in the high half, a count of finished final-consumer workgroups in
+// the low half. The count is spread over kDoneWords words kDoneStride words
+// apart (each in a 128-byte line of its own): workgroup b counts in word
+// b % kDoneWords, so that at most ceil(grid / kDoneWords) device-scope adds
+// meet on one address (256 adds on one word took ~8 us to drain).
+constexpr int kDoneWords = 8;
+constexpr int kDoneStride = 32;
 __host__ __device__ inline uint32_t done_tag_of(uint32_t seq) { return (seq & 0xFFFFu) << 16; }
+// Workgroups b < blocks with b % kDoneWords == k.
+__host__ __device__ inline uint32_t done_share(int32_t blocks, int k) {
+    return blocks > k ? (uint32_t)((blocks - 1 - k) / kDoneWords + 1) : 0u;
+}
+// One wave that polls the done words until word k reaches done_tag plus
+// done_share(blocks, k) for every k (bounded like launch_wait).
+hipError_t launch_done_wait(const uint32_t* done, uint32_t done_tag, int32_t blocks, uint32_t* status,
+                            uint64_t timeout_ticks, hipStream_t s);
 hipError_t launch_gate(uint32_t* gate, uint32_t tag, uint32_t* status, uint64_t timeout_ticks, hipStream_t s);
 
 }  // namespace fo

@@ -87,6 +87,26 @@ __global__ __launch_bounds__(64) void wait_kernel(const uint32_t* counter, uint3
     }
 }
 
+// End handoff of an overlapped run (one wave, on the GEMM stream ahead of the
+// post-reorder): lane k < kDoneWords polls done word k until it reaches the
+// run's tag plus its share of the final launch's workgroups; the wave ends
+// when every lane's word has. Bounded like wait_kernel.
+__global__ __launch_bounds__(64) void done_wait_kernel(const uint32_t* done, uint32_t done_tag, int32_t blocks,
+                                                       uint32_t* status, uint64_t timeout_ticks) {
+    const int k = threadIdx.x;
+    const bool mine = k < kDoneWords;
+    const uint32_t target = done_tag + done_share(blocks, k);
+    const uint32_t* w = done + (mine ? k : 0) * kDoneStride;
+    const uint64_t t0 = wall_clock64();
+    while (!__all(!mine || __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target)) {
+        __builtin_amdgcn_s_sleep(8);
+        if (wall_clock64() - t0 > timeout_ticks) {
+            if (k == 0 && status) __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return;
+        }
+    }
+}
+
 // Start handoff of an overlapped run (one wave, on the consumer stream ahead
 // of the run's first consumer): lane 0 polls the gate word until it holds
 // the run's tag, which the run's reset kernel writes with a release once the
@@ -344,9 +364,10 @@ __global__ __launch_bounds__(kMaxThreads) void consume_kernel(const ConsumeArgs 
             // microsecond each. A late workgroup can only race with a later
             // run's reset if an earlier wait of the stream pair timed out,
             // which the sticky status bit already reports.)
-            const uint32_t v = __hip_atomic_load(a.done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            uint32_t* w = a.done + (blockIdx.x % kDoneWords) * kDoneStride;
+            const uint32_t v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if ((v & 0xFFFF0000u) == a.done_tag)
-                __hip_atomic_fetch_add(a.done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_fetch_add(w, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 }
@@ -380,6 +401,12 @@ void launch_unroll(bool full, int sync, int path, dim3 g, dim3 b, hipStream_t s,
 hipError_t launch_wait(const uint32_t* counter, uint32_t target, uint32_t* status, uint64_t timeout_ticks,
                        hipStream_t s) {
     hipLaunchKernelGGL(wait_kernel, dim3(1), dim3(64), 0, s, counter, target, status, timeout_ticks);
+    return hipGetLastError();
+}
+
+hipError_t launch_done_wait(const uint32_t* done, uint32_t done_tag, int32_t blocks, uint32_t* status,
+                            uint64_t timeout_ticks, hipStream_t s) {
+    hipLaunchKernelGGL(done_wait_kernel, dim3(1), dim3(64), 0, s, done, done_tag, blocks, status, timeout_ticks);
     return hipGetLastError();
 }
 

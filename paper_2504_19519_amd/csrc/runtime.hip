@@ -121,14 +121,17 @@ fo_status clock_khz(int64_t* out) {
     return FO_OK;
 }
 
+static_assert(FO_HANDOFF_WORDS == 2 + (kDoneWords - 1) * kDoneStride,
+              "handoff words: the gate word, then kDoneWords done words kDoneStride apart");
+
 __global__ void fill_u32_kernel(uint32_t* p, int32_t n, uint32_t v) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n) p[i] = v;
 }
 
 // Start of an overlapped run, one workgroup on the GEMM stream: zero the
-// group and position counters (n words), set the done word to the run's
-// done tag with a count of zero, make both visible device-wide, then
+// group and position counters (n words), set the kDoneWords done words to
+// the run's done tag with a count of zero, make both visible device-wide, then
 // exchange the gate word for the run's tag (the start handoff that the gate
 // kernel on the consumer stream waits for). If a gate of this run timed out
 // before, the word holds the tag's timed-out mark: the status word then gets
@@ -138,7 +141,7 @@ __global__ __launch_bounds__(256) void reset_run_kernel(uint32_t* counters, int3
                                                         uint32_t done_tag, uint32_t* status, uint32_t* gate,
                                                         uint32_t tag) {
     for (int i = threadIdx.x; i < n; i += blockDim.x) counters[i] = 0u;
-    if (threadIdx.x == 0 && done) *done = done_tag;
+    if (done && threadIdx.x < kDoneWords) done[threadIdx.x * kDoneStride] = done_tag;
     if (!gate) return;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
@@ -462,7 +465,7 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
     const uint64_t ticks = a.timeout_ticks;
     // Handoff words after the group and position counters.
     uint32_t* gate = overlap ? counters + plan->P + FO_DISPENSER_WORDS : nullptr;
-    uint32_t* done = overlap ? gate + 1 : nullptr;
+    uint32_t* done = overlap ? gate + 1 : nullptr;      // done word 0; word k at done + k * kDoneStride
     const uint32_t seq = fo::g_run_seq.fetch_add(1, std::memory_order_relaxed);
     const uint32_t tag = fo::kGateTag | (seq & fo::kGateSeqMask);
     const uint32_t done_tag = fo::done_tag_of(seq);
@@ -485,7 +488,7 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
     // group. Groups before the last one share the device with the GEMM and
     // use the configured grid cap; the last group runs once the GEMM is
     // done and takes the full grid. The final launch counts its finished
-    // workgroups in the done word, for which the GEMM stream waits before
+    // workgroups in the done words, for which the GEMM stream waits before
     // the post-reorder.
     const int64_t* seg = plan->segs.data();
     const int nseg = (int)(plan->segs.size() / 5);
@@ -525,11 +528,11 @@ fo_status fo_run_overlapped(const fo_plan* plan, const void* dev_plan, const voi
                                     final_launch ? &final_blocks : nullptr)) != hipSuccess)
             return fo::hip_fail("consumer launch", e);
     }
-    // the done word reaches the run's tag plus the launch's grid only through
-    // this run's final consumer (a late consumer of an earlier run finds
-    // another tag in it and does not count)
+    // the done words reach the run's tag plus their shares of the launch's
+    // grid only through this run's final consumer (a late consumer of an
+    // earlier run finds another tag in them and does not count)
     if (final_blocks > 0 &&
-        (e = fo::launch_wait(done, done_tag + (uint32_t)final_blocks, status_word, ticks, s1)) != hipSuccess)
+        (e = fo::launch_done_wait(done, done_tag, final_blocks, status_word, ticks, s1)) != hipSuccess)
         return fo::hip_fail("wait kernel launch", e);
     if (out) return fo_post_reorder(plan, dev_plan, dst, out, bias, gamma, eps, do_rmsnorm, s1);
     return FO_OK;

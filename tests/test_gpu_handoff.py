@@ -5,7 +5,7 @@ the GEMM stream writes the run's tag into a gate word that a one-wave kernel
 on the consumer stream waits for (so the consumers of a run start only after
 the counters are zero and the previous run's post-reorder has read the
 destination buffer), and the final consumer launch counts its finished
-workgroups into a done word that a one-wave wait on the GEMM stream checks
+workgroups into done words that a one-wave wait on the GEMM stream checks
 before the post-reorder (so the post-reorder reads complete groups and the
 next GEMM does not overwrite what a consumer still reads). These tests run
 back-to-back runs that share every buffer but their outputs, hold either

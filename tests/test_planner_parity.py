@@ -282,7 +282,7 @@ def test_given_partition_estimate_matches_oracle(seed, pattern, nd):
 def test_counters_and_overlapped_argument_checks():
     # host-side checks only: these calls return before any device work
     p = fo.plan_groups(1024, 1024, 64, sizes=[2, 2], num_cus=8, tile_m=256, tile_n=128)   # 32 tiles, 4 waves
-    assert p.num_counters == p.P + 8 + 2          # groups, positions, handoff words
+    assert p.num_counters == p.P + 8 + 226        # groups, positions, handoff words
     fake = 1 << 20                                # never dereferenced
     for kw in (dict(counters=None, gemm_stream=fake, comm_stream=fake + 64),   # no counters
                dict(counters=fake, gemm_stream=None, comm_stream=fake + 64)):  # null GEMM stream
