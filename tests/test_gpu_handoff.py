@@ -186,6 +186,37 @@ def test_a_timed_out_run_does_not_count_for_the_next():
     np.testing.assert_array_equal(st.counters.cpu().numpy()[:st.plan.P], np.array(st.o.targets))
 
 
+def test_stale_counter_words_do_not_reach_a_run():
+    # group and position counters left dirty by some earlier user of the
+    # array (values below, at and far past every class's positions): an
+    # overlapped run zeroes them on its GEMM stream before the GEMM and the
+    # consumers use them, so its output is whole; a standalone GEMM launch
+    # after fo_reset_counters is whole as well
+    torch = torch_mod()
+    say("[handoff stale counters] rs_8192x8192x3584 small")
+    st = Setup("rs_8192x8192x3584")
+    P = st.plan.P
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    for k, junk in enumerate([3, 1 << 20, 0x7FFFFFF0]):
+        st.counters[:P + fo.DISPENSER_WORDS] = junk
+        torch.cuda.synchronize()
+        out = empty16(st.w.M * st.w.N, st.w.dtype)
+        st.run(k, out, s1, s2)
+        torch.cuda.synchronize()
+        assert int(st.status.cpu()[0]) == 0, f"junk {junk}"
+        st.check(k, out)
+        np.testing.assert_array_equal(st.counters.cpu().numpy()[:P], np.array(st.o.targets))
+        np.testing.assert_array_equal(st.counters.cpu().numpy()[P:P + fo.DISPENSER_WORDS], 0)
+    # standalone: fo_reset_counters clears what a dirty array holds
+    st.counters[:P + fo.DISPENSER_WORDS] = 5
+    fo.reset_counters(st.counters, P + fo.DISPENSER_WORDS)
+    C = empty16(st.w.M * st.w.N)
+    fo.gemm_signal_reorder(st.plan, st.dp, st.A[0], st.W, C, st.counters)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(st.counters.cpu().numpy()[:P], np.array(st.o.targets))
+    np.testing.assert_array_equal(st.counters.cpu().numpy()[P:P + fo.DISPENSER_WORDS], 0)
+
+
 def test_back_to_back_runs_at_full_size():
     # the bench's configuration: rs 8192x8192x3584, 256 CUs, waves [1, 2, 1];
     # three runs without host synchronisation, alternating two A operands,
