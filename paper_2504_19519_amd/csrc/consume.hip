@@ -190,17 +190,24 @@ __device__ __forceinline__ uint16_t add1(uint16_t x, uint16_t y) {
     return (uint16_t)from_f32<DT>(to_f32<DT>(x) + to_f32<DT>(y));
 }
 
+// The streaming functions take the thread's first unit index in the segment
+// in `i0` (below the grid size) and leave there its first index in the next segment: the grid-stride
+// sequence runs on across the launch's segments as if they were one buffer, so the threads that take a segment's last partial round start
+// the next one later and every thread ends up with the same share of the
+// group (restarting each segment at the thread's own index left the
+// low-numbered threads with one extra, latency-bound round per segment).
+
 // Stream one segment, 16 bytes per lane per access (FENCE_ALL / FENCE_ONE;
 // src, peer and dst 16-byte aligned): nontemporal loads and stores.
 template <int DT, bool SUM, int kUnroll, bool WT>
 __device__ __forceinline__ void stream_vec16(const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer,
-                                             uint16_t* __restrict__ dst, int64_t len) {
+                                             uint16_t* __restrict__ dst, int64_t len, uint32_t& i0) {
+    int64_t i = i0;
     const int64_t n16 = len >> 3;
     const u32x4_t* s = reinterpret_cast<const u32x4_t*>(src);
     const u32x4_t* q = reinterpret_cast<const u32x4_t*>(peer);
     u32x4_t* d = reinterpret_cast<u32x4_t*>(dst);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     for (; i + (kUnroll - 1) * stride < n16; i += kUnroll * stride) {
         u32x4_t x[kUnroll], y[kUnroll];
 #pragma unroll
@@ -219,6 +226,7 @@ __device__ __forceinline__ void stream_vec16(const uint16_t* __restrict__ src, c
         if constexpr (SUM) x = add8<DT>(x, __builtin_nontemporal_load(q + i));
         put16<WT>(d + i, x);
     }
+    i0 = (uint32_t)(i - n16);
     // ragged tail (< 8 elements)
     if (blockIdx.x == 0 && threadIdx.x < (len & 7)) {
         const int64_t e = (n16 << 3) + threadIdx.x;
@@ -232,14 +240,14 @@ __device__ __forceinline__ void stream_vec16(const uint16_t* __restrict__ src, c
 template <int DT, bool SUM, int kUnroll, bool WT>
 __device__ __forceinline__ void stream_coherent8(const uint16_t* __restrict__ src,
                                                  const uint16_t* __restrict__ peer,
-                                                 uint16_t* __restrict__ dst, int64_t len) {
+                                                 uint16_t* __restrict__ dst, int64_t len, uint32_t& i0) {
+    int64_t i = i0;
     constexpr int U = 2 * kUnroll;
     const int64_t n8 = len >> 2;
     const uint64_t* s = reinterpret_cast<const uint64_t*>(src);
     const uint64_t* q = reinterpret_cast<const uint64_t*>(peer);
     uint64_t* d = reinterpret_cast<uint64_t*>(dst);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     auto add4 = [](uint64_t x, uint64_t y) -> uint64_t {
         u32x4_t a, b;
         a[0] = (uint32_t)x; a[1] = (uint32_t)(x >> 32); a[2] = 0; a[3] = 0;
@@ -266,6 +274,7 @@ __device__ __forceinline__ void stream_coherent8(const uint16_t* __restrict__ sr
         if constexpr (SUM) x = add4(x, __builtin_nontemporal_load(q + i));
         put8<WT>(d + i, x);
     }
+    i0 = (uint32_t)(i - n8);
     // ragged tail (< 4 elements): an acquire, then plain 2-byte loads
     if (blockIdx.x == 0 && threadIdx.x < (len & 3)) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
@@ -284,7 +293,8 @@ __device__ __forceinline__ void stream_coherent8(const uint16_t* __restrict__ sr
 template <int DT, bool SUM, int kUnroll, bool WT>
 __device__ __forceinline__ void stream_coherent16(const uint16_t* __restrict__ src,
                                                   const uint16_t* __restrict__ peer,
-                                                  uint16_t* __restrict__ dst, int64_t len) {
+                                                  uint16_t* __restrict__ dst, int64_t len, uint32_t& i0) {
+    int64_t i = i0;
     constexpr int kSc1Nt = 16 | 2;   // cache policy operand: sc1, nt
     const __amdgpu_buffer_rsrc_t rs =
         __builtin_amdgcn_make_buffer_rsrc((void*)src, 0, (int)(len * 2), kRsrcWord3);
@@ -292,7 +302,6 @@ __device__ __forceinline__ void stream_coherent16(const uint16_t* __restrict__ s
     const u32x4_t* q = reinterpret_cast<const u32x4_t*>(peer);
     u32x4_t* d = reinterpret_cast<u32x4_t*>(dst);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     for (; i + (kUnroll - 1) * stride < n16; i += kUnroll * stride) {
         u32x4_t x[kUnroll], y[kUnroll];
 #pragma unroll
@@ -312,6 +321,7 @@ __device__ __forceinline__ void stream_coherent16(const uint16_t* __restrict__ s
         if constexpr (SUM) x = add8<DT>(x, __builtin_nontemporal_load(q + i));
         put16<WT>(d + i, x);
     }
+    i0 = (uint32_t)(i - n16);
     // ragged tail (< 8 elements): an acquire, then plain 2-byte loads
     if (blockIdx.x == 0 && threadIdx.x < (len & 7)) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
@@ -323,10 +333,12 @@ __device__ __forceinline__ void stream_coherent16(const uint16_t* __restrict__ s
 // Stream one segment element by element (unaligned buffers).
 template <int DT, bool SUM, bool WT>
 __device__ __forceinline__ void stream_elem(const uint16_t* __restrict__ src, const uint16_t* __restrict__ peer,
-                                            uint16_t* __restrict__ dst, int64_t len) {
+                                            uint16_t* __restrict__ dst, int64_t len, uint32_t& i0) {
+    int64_t i = i0;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += stride)
+    for (; i < len; i += stride)
         put2<WT>(dst + i, SUM ? add1<DT>(src[i], peer[i]) : src[i]);
+    i0 = (uint32_t)(i - len);
 }
 
 enum { kPathVec16 = 0, kPathCoherent8 = 1, kPathElem = 2, kPathCoherent16 = 3 };
@@ -342,15 +354,16 @@ enum { kPathVec16 = 0, kPathCoherent8 = 1, kPathElem = 2, kPathCoherent16 = 3 };
 template <int DT, bool SUM, int SYNC, int PATH, int U, bool WT>
 __global__ __launch_bounds__(kMaxThreads) void consume_kernel(const ConsumeArgs a) {
     if (!a.counter || check_counter<SYNC>(a.counter, a.target, a.status)) {
+        uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;   // < grid size: fits 32 bits
         for (int k = 0; k < a.nseg; ++k) {
             const ConsumeSegment g = a.seg[k];
             const uint16_t* src = a.src + g.src_off;
             const uint16_t* peer = SUM ? a.peer + g.src_off : nullptr;
             uint16_t* dst = a.dst + g.dst_off;
-            if constexpr (PATH == kPathVec16) stream_vec16<DT, SUM, U, WT>(src, peer, dst, g.len);
-            else if constexpr (PATH == kPathCoherent16) stream_coherent16<DT, SUM, U, WT>(src, peer, dst, g.len);
-            else if constexpr (PATH == kPathCoherent8) stream_coherent8<DT, SUM, U, WT>(src, peer, dst, g.len);
-            else stream_elem<DT, SUM, WT>(src, peer, dst, g.len);
+            if constexpr (PATH == kPathVec16) stream_vec16<DT, SUM, U, WT>(src, peer, dst, g.len, i);
+            else if constexpr (PATH == kPathCoherent16) stream_coherent16<DT, SUM, U, WT>(src, peer, dst, g.len, i);
+            else if constexpr (PATH == kPathCoherent8) stream_coherent8<DT, SUM, U, WT>(src, peer, dst, g.len, i);
+            else stream_elem<DT, SUM, WT>(src, peer, dst, g.len, i);
         }
     }
     if constexpr (WT) {
@@ -372,12 +385,19 @@ __global__ __launch_bounds__(kMaxThreads) void consume_kernel(const ConsumeArgs 
     }
 }
 
+// Unroll of the 8-byte coherent path: a bf16 sum of 4 x 2 units per thread
+// in flight takes ~87 registers, more than a SIMD running a 256x256 GEMM wave
+// leaves free, so that case issues 2 x 2.
+template <int DT, int U>
+constexpr int kUnit8Unroll = (DT == FO_BF16 && U > kUnrollBeside) ? kUnrollBeside : U;
+
 template <int DT, bool SUM, int U, bool WT>
 void launch_variant(int sync, int path, dim3 g, dim3 b, hipStream_t s, const ConsumeArgs& a) {
     if (path == kPathCoherent16)
         hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent16, U, WT>), g, b, 0, s, a);
-    else if (path == kPathCoherent8)
-        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent8, U, WT>), g, b, 0, s, a);
+    else if (path == kPathCoherent8)   // bf16 sums: fewer 8-byte units in flight (the budget of registers)
+        hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_COHERENT, kPathCoherent8, kUnit8Unroll<DT, U>, WT>), g,
+                           b, 0, s, a);
     else if (path == kPathVec16 && sync == FO_SYNC_FENCE_ALL)
         hipLaunchKernelGGL((consume_kernel<DT, SUM, FO_SYNC_FENCE_ALL, kPathVec16, U, WT>), g, b, 0, s, a);
     else if (path == kPathVec16)
@@ -388,12 +408,16 @@ void launch_variant(int sync, int path, dim3 g, dim3 b, hipStream_t s, const Con
 
 // A counting launch (a.done) is the last group's; it takes the unroll its
 // `full` flag asks for like any other launch.
+// A copy has one load per unit where a sum has two, so it unrolls twice as
+// far for the same bytes in flight per thread.
 template <int DT, bool SUM>
 void launch_unroll(bool full, int sync, int path, dim3 g, dim3 b, hipStream_t s, const ConsumeArgs& a) {
-    if (a.done && full) launch_variant<DT, SUM, kUnrollFull, true>(sync, path, g, b, s, a);
-    else if (a.done) launch_variant<DT, SUM, kUnrollBeside, true>(sync, path, g, b, s, a);
-    else if (full) launch_variant<DT, SUM, kUnrollFull, false>(sync, path, g, b, s, a);
-    else launch_variant<DT, SUM, kUnrollBeside, false>(sync, path, g, b, s, a);
+    constexpr int kFull = SUM ? kUnrollFull : 2 * kUnrollFull;
+    constexpr int kBeside = SUM ? kUnrollBeside : 2 * kUnrollBeside;
+    if (a.done && full) launch_variant<DT, SUM, kFull, true>(sync, path, g, b, s, a);
+    else if (a.done) launch_variant<DT, SUM, kBeside, true>(sync, path, g, b, s, a);
+    else if (full) launch_variant<DT, SUM, kFull, false>(sync, path, g, b, s, a);
+    else launch_variant<DT, SUM, kBeside, false>(sync, path, g, b, s, a);
 }
 
 }  // namespace
