@@ -52,6 +52,23 @@ OTHER_WORKLOADS = ("tiny", "ar_2048x4096x4096", "ar_rmsnorm_16384x4096x3584_bf16
 OPTS = None
 
 
+# The run's streams, created once: the GEMM stream, the consumer stream and
+# one more for a GEMM that a consumer measurement runs beside. HIP maps
+# streams onto a few hardware queues per device (GPU_MAX_HW_QUEUES, 4 by
+# default); each new pair of streams in a process risks sharing a queue
+# with another stream, and kernels of one queue do not overlap (measured:
+# a second stream pair in the process took a2a_4096x7168x2048 from 147 to
+# 164 us per step), so every phase reuses these.
+_STREAMS = None
+
+
+def streams(torch):
+    global _STREAMS
+    if _STREAMS is None:
+        _STREAMS = tuple(torch.cuda.Stream() for _ in range(3))
+    return _STREAMS
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -267,7 +284,7 @@ def consumer_curve(torch, w, b, stream, total_elems, beside=None):
     if beside is None:
         return [2.0 * n for n in sizes], [time_loop(torch, lambda: launch(n), 20, 3, stream) for n in sizes]
     plan, dp = beside
-    sg = torch.cuda.Stream()
+    sg = streams(torch)[2]
     ys = []
     for n in sizes:
         vals = []
@@ -489,7 +506,7 @@ def workload_summary(torch, name, num_cus, steps):
     inp = workloads.make_inputs(w)
     tiles = (w.M // w.tile_m) * (w.N // w.tile_n)
     T = -(-tiles // num_cus)
-    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    s1, s2, _ = streams(torch)
     if w.groups is not None:
         base_plan = make_plan(w, inp, num_cus, sizes=list(w.groups)) if w.group_unit == "waves" else \
             fo.plan_groups(w.M, w.N, w.K, dtype=w.dtype, tile_m=w.tile_m, tile_n=w.tile_n, order=w.order,
@@ -810,7 +827,7 @@ def predictor_breadth(torch, w, num_cus, steps):
         inp = workloads.make_inputs(ws)
         tiles = (ws.M // ws.tile_m) * (ws.N // ws.tile_n)
         T = -(-tiles // num_cus)
-        s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+        s1, s2, _ = streams(torch)
         base_plan = make_plan(ws, inp, num_cus, sizes=[1] * T)
         b = Bufs(torch, ws, inp, base_plan.dest_elems)
         dp_base = dev_plan(torch, base_plan)
@@ -856,7 +873,7 @@ def main():
     tiles = (w.M // w.tile_m) * (w.N // w.tile_n)
     T = -(-tiles // num_cus)
     flops = w.flops
-    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    s1, s2, _ = streams(torch)
 
     plan_rm = make_plan(w, inp, num_cus, sizes=[1] * T, pattern="rowmajor")
     base_plan = make_plan(w, inp, num_cus, sizes=[1] * T)

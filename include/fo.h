@@ -422,6 +422,12 @@ fo_status fo_reset_counters(uint32_t* counters, int32_t n, void* stream);
  * way (counters untouched). An overlapped run needs counters and,
  * with more than one group, a created gemm_stream (not the null stream,
  * which would wait for the gate kernel on a blocking comm_stream).
+ * The overlap also needs the two streams on different hardware queues: HIP
+ * maps streams onto a few queues per device (GPU_MAX_HW_QUEUES, 4 by
+ * default), and kernels of streams that share a queue run one after another.
+ * The run is then serialized but still correct (each handoff waits only for
+ * work enqueued before it); a process that keeps creating streams should
+ * reuse one pair for its overlapped runs.
  * Buffers: C_out (GEMM output, see fo_gemm_signal_reorder), peer (NULL for
  * All-to-All; else the peer's partial in C_out's layout), dst
  * (fo_plan_dest_elems), out ([M, N] or NULL), counters

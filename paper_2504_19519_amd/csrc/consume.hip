@@ -385,11 +385,12 @@ __global__ __launch_bounds__(kMaxThreads) void consume_kernel(const ConsumeArgs 
     }
 }
 
-// Unroll of the 8-byte coherent path: a bf16 sum of 4 x 2 units per thread
-// in flight takes ~87 registers, more than a SIMD running a 256x256 GEMM wave
-// leaves free, so that case issues 2 x 2.
+// Unroll of the 8-byte coherent path (outputs past a 31-bit byte range): at
+// most 4 x 2 units per thread in flight, 2 x 2 for bf16, whose sums need
+// more registers (4 x 2 bf16 units took ~87 registers, more than a SIMD
+// running a 256x256 GEMM wave leaves free).
 template <int DT, int U>
-constexpr int kUnit8Unroll = (DT == FO_BF16 && U > kUnrollBeside) ? kUnrollBeside : U;
+constexpr int kUnit8Unroll = DT == FO_BF16 ? (U < 2 ? U : 2) : (U < 4 ? U : 4);
 
 template <int DT, bool SUM, int U, bool WT>
 void launch_variant(int sync, int path, dim3 g, dim3 b, hipStream_t s, const ConsumeArgs& a) {
