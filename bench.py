@@ -27,6 +27,7 @@ bounded sample).
 from __future__ import annotations
 
 import argparse
+import ctypes
 import dataclasses
 import json
 import os
@@ -67,6 +68,60 @@ def streams(torch):
     if _STREAMS is None:
         _STREAMS = tuple(torch.cuda.Stream() for _ in range(3))
     return _STREAMS
+
+
+class Ev:
+    """A HIP event of the process's HIP runtime (the one torch loaded). For
+    timing marks it is created with hipEventDisableSystemFence: recording it
+    then does not write back and invalidate the caches, which would add to
+    the interval it brackets (a GEMM bracketed by torch's events measured ~8
+    us longer than its kernel trace). fence=True: a default event, for one
+    that another stream waits on."""
+    _hip = None
+
+    @classmethod
+    def _lib(cls):
+        if cls._hip is None:
+            with open("/proc/self/maps") as f:
+                paths = sorted({ln.split()[-1] for ln in f if ln.rstrip().endswith(".so") and
+                                os.path.basename(ln.split()[-1]).startswith("libamdhip64")})
+            assert paths, "the HIP runtime is not loaded"
+            h = ctypes.CDLL(paths[0])
+            vp = ctypes.c_void_p
+            h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(vp), ctypes.c_uint]
+            h.hipEventRecord.argtypes = [vp, vp]
+            h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), vp, vp]
+            h.hipEventDestroy.argtypes = [vp]
+            h.hipStreamWaitEvent.argtypes = [vp, vp, ctypes.c_uint]
+            cls._hip = h
+        return cls._hip
+
+    def __init__(self, fence=False):
+        h = ctypes.c_void_p()
+        rc = self._lib().hipEventCreateWithFlags(ctypes.byref(h), 0 if fence else 0x20000000)
+        assert rc == 0, f"hipEventCreateWithFlags: {rc}"
+        self.cuda_event = h.value
+
+    def record(self, stream):
+        rc = self._lib().hipEventRecord(self.cuda_event, stream.cuda_stream)
+        assert rc == 0, f"hipEventRecord: {rc}"
+
+    def elapsed_time(self, end):
+        ms = ctypes.c_float()
+        rc = self._lib().hipEventElapsedTime(ctypes.byref(ms), self.cuda_event, end.cuda_event)
+        assert rc == 0, f"hipEventElapsedTime: {rc}"
+        return ms.value
+
+    def wait(self, stream):
+        rc = self._lib().hipStreamWaitEvent(stream.cuda_stream, self.cuda_event, 0)
+        assert rc == 0, f"hipStreamWaitEvent: {rc}"
+
+    def __del__(self):
+        try:
+            if self.cuda_event and Ev._hip is not None:
+                Ev._hip.hipEventDestroy(self.cuda_event)
+        except Exception:      # interpreter shutdown
+            pass
 
 
 def log(msg):
@@ -130,7 +185,7 @@ def time_loop(torch, fn, iters, warmup, stream):
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0, e1 = Ev(), Ev()
     e0.record(stream)
     for _ in range(iters):
         fn()
@@ -145,8 +200,7 @@ def time_gemm(torch, plan, dp, b, stream, iters, warmup, signal=True, opts=None)
     (outside the events) and the GEMM signals them, taking its positions from
     the dispensers; signal=False: no counters (static schedule, plain
     stores)."""
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(iters)]
+    ev = [(Ev(), Ev()) for _ in range(iters)]
 
     def one(pair=None):
         if signal:
@@ -219,16 +273,15 @@ def timed_steps(torch, w, plan, dp, b, s1, s2, steps, warmup):
     events on s1 (s1 joins s2 before the post-reorder of every step). A
     second, untimed pass of the same steps brackets each GEMM launch with an
     event pair for the GEMM's duration inside the step; those events stay out
-    of the timed pass, as their system-scope fences would add to its time."""
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)]
+    of the timed pass, as recording them would add to its time."""
+    ev = [(Ev(), Ev()) for _ in range(steps)]
     for a, c in ev:          # create the events
         a.record(s1)
         c.record(s1)
     for _ in range(warmup):
         run_step(torch, w, plan, dp, b, s1, s2)
     torch.cuda.synchronize()
-    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0, t1 = Ev(), Ev()
     wall0 = time.perf_counter()
     t0.record(s1)
     for k in range(steps):
@@ -289,11 +342,11 @@ def consumer_curve(torch, w, b, stream, total_elems, beside=None):
     for n in sizes:
         vals = []
         for r in range(6):
-            eg, e0, e1 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            eg, e0, e1 = Ev(fence=True), Ev(), Ev()
             eg.record(sg)
             for _ in range(2):        # about 700 us of GEMM for the consumer to run beside
                 fo.gemm_signal_reorder(plan, dp, b.A, b.W, b.C, None, sg)
-            stream.wait_event(eg)
+            eg.wait(stream)
             e0.record(stream)
             launch(n)
             e1.record(stream)
@@ -326,12 +379,12 @@ def consumer_curve_after(torch, w, b, inp, num_cus, s1, s2, total_elems):
     for n in sizes:
         vals = []
         for r in range(5):
-            er, eg, e1 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            er, eg, e1 = Ev(fence=True), Ev(), Ev()
             fo.reset_counters(b.counters, one.num_counters, s1)
             er.record(s1)
             fo.gemm_signal_reorder(one, dp, b.A, b.W, b.C, b.counters, s1)
             eg.record(s1)
-            s2.wait_event(er)
+            er.wait(s2)
             fo.consume_group(b.C, b.peer, b.dst, n, w.dtype, b.counters, int(one.targets[0]), b.status, s2,
                              opts=full)
             e1.record(s2)
@@ -348,8 +401,7 @@ def gemm_comm_times(torch, w, plan, dp, b, s1, s2, steps, with_gemm=False):
     the GEMM's start (event on the GEMM stream) to the end of the last
     consumer (event on the stream it ran on: the communication stream, or
     the GEMM stream for a plan of one group, which runs serialized)."""
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-           torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    ev = [(Ev(), Ev(), Ev()) for _ in range(steps)]
     last = s2 if plan.P > 1 else s1
     for a, g, c in ev:       # create the events
         a.record(s1)
