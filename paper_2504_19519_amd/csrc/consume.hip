@@ -191,11 +191,12 @@ __device__ __forceinline__ uint16_t add1(uint16_t x, uint16_t y) {
 }
 
 // The streaming functions take the thread's first unit index in the segment
-// in `i0` (below the grid size) and leave there its first index in the next segment: the grid-stride
-// sequence runs on across the launch's segments as if they were one buffer, so the threads that take a segment's last partial round start
-// the next one later and every thread ends up with the same share of the
-// group (restarting each segment at the thread's own index left the
-// low-numbered threads with one extra, latency-bound round per segment).
+// in `i0` (below the grid size) and leave there its first index in the next
+// segment: the grid-stride sequence runs on across the launch's segments as
+// if they were one buffer, so the threads that take a segment's last partial
+// round start the next one later and every thread ends up with the same
+// share of the group (restarting each segment at the thread's own index left
+// the low-numbered threads with one extra, latency-bound round per segment).
 
 // Stream one segment, 16 bytes per lane per access (FENCE_ALL / FENCE_ONE;
 // src, peer and dst 16-byte aligned): nontemporal loads and stores.
