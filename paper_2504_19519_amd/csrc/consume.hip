@@ -460,8 +460,12 @@ hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blo
     const int path = sync == FO_SYNC_COHERENT
                          ? (vec16 && fits32 ? kPathCoherent16 : vec8 ? kPathCoherent8 : kPathElem)
                          : (vec16 ? kPathVec16 : kPathElem);
-    const int unroll = full ? kUnrollFull : kUnrollBeside;
-    const int64_t per_block = path == kPathCoherent8 ? (int64_t)threads * 2 * unroll * 4
+    // elements one workgroup moves per unrolled round (the unrolls of
+    // launch_unroll and kUnit8Unroll), for the grid of a short launch
+    const bool sum = a.peer != nullptr;
+    const int unroll = (full ? kUnrollFull : kUnrollBeside) * (sum ? 1 : 2);
+    const int unroll8 = dtype == FO_BF16 ? (unroll < 2 ? unroll : 2) : (unroll < 4 ? unroll : 4);
+    const int64_t per_block = path == kPathCoherent8 ? (int64_t)threads * 2 * unroll8 * 4
                               : path == kPathVec16 || path == kPathCoherent16 ? (int64_t)threads * unroll * 8
                                                                                : (int64_t)threads;
     int64_t blocks = (total + per_block - 1) / per_block;
@@ -474,7 +478,6 @@ hipError_t launch_consume(int dtype, int sync, const ConsumeArgs& a, int max_blo
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    const bool sum = a.peer != nullptr;
     if (dtype == FO_FP16) {
         if (sum) launch_unroll<FO_FP16, true>(full, sync, path, g, b, s, a);
         else launch_unroll<FO_FP16, false>(full, sync, path, g, b, s, a);
