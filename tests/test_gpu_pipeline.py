@@ -164,6 +164,56 @@ def test_small_workloads(name):
         assert np.all(np.abs(y - r) <= bound), "end to end (bf16 bound)"
 
 
+def _composition(rng, total, parts):
+    cuts = sorted(rng.choice(np.arange(1, total), size=parts - 1, replace=False)) if parts > 1 else []
+    b = [0] + [int(c) for c in cuts] + [total]
+    return [b[i + 1] - b[i] for i in range(parts)]
+
+
+def random_cases(n, seed=2504):
+    """Seeded random small paths: tile shape, M / N / K, dtype, dispatch order,
+    pattern and destination count, bias / RMSNorm / gamma, modelled CU count
+    and a partition in waves or in tiles (mostly several groups)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for k in range(n):
+        tm, tn = [(256, 128), (256, 256), (64, 64)][int(rng.integers(3))]
+        M, N, K = tm * int(rng.integers(1, 7)), tn * int(rng.integers(1, 7)), 64 * int(rng.integers(1, 9))
+        pattern = ["tile", "subtile", "subtoken"][int(rng.integers(3))]
+        nd = (int(rng.choice([2, 4, 8])) if pattern == "subtile" else
+              int(rng.integers(2, 9)) if pattern == "subtoken" else 2)
+        rms, bias = bool(rng.integers(2)), bool(rng.integers(2))
+        gamma = rms and bool(rng.integers(2))
+        w = workloads.Workload(name=f"random{k}", M=M, N=N, K=K, dtype=["fp16", "bf16"][int(rng.integers(2))],
+                               tile_m=tm, tile_n=tn, order=["xcd", "rowmajor"][int(rng.integers(2))],
+                               pattern=pattern, seed=100 + k, dist="uniform", num_dest=nd,
+                               bias=bias, rmsnorm=rms, gamma=gamma)
+        cus = int(rng.choice([2, 3, 5, 8]))
+        tiles = (M // tm) * (N // tn)
+        T = -(-tiles // cus)
+        if rng.integers(3) == 0 and tiles > 1:
+            unit, sizes = "tiles", _composition(rng, tiles, int(rng.integers(min(2, tiles), min(5, tiles) + 1)))
+        else:
+            unit = "waves"
+            sizes = _composition(rng, T, int(rng.integers(2, min(5, T) + 1))) if T > 1 else [1]
+        out.append((w, cus, sizes, unit))
+    return out
+
+
+@pytest.mark.parametrize("case", range(40))
+def test_random_paths(case):
+    # the whole path on seeded random small shapes: every check of
+    # test_small_workloads' first part (GEMM against the exact product,
+    # reorder, consumer and post-reorder against the oracle, serialized run
+    # equal to the overlapped one)
+    w, cus, sizes, unit = random_cases(40)[case]
+    say(f"[pipeline random] {w.name} {w.M}x{w.N}x{w.K} {w.dtype} tile {w.tile_m}x{w.tile_n} {w.order} "
+        f"{w.pattern}/{w.num_dest} bias={w.bias} rms={w.rmsnorm} gamma={w.gamma} cus={cus} {unit} {sizes}")
+    inp = workloads.make_inputs(w)
+    plan, o = plan_for(w, inp, num_cus=cus, sizes=sizes, unit=unit)
+    check(w, inp, plan, o)
+
+
 FULL = {
     "ar_2048x4096x4096": [(1,)],
     "rs_8192x8192x3584": [(1,) * 4, (2, 2), (1, 3)],
