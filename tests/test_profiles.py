@@ -30,7 +30,8 @@ def test_every_large_workload_has_a_summary():
         assert os.path.exists(os.path.join(ROOT, "profiles", f"serial_step_and_gemm_{n}.md"))
 
 
-@pytest.mark.parametrize("path", STEP + sorted(glob.glob(os.path.join(ROOT, "profiles", "serial_step_*.md"))))
+@pytest.mark.parametrize("path", STEP + sorted(glob.glob(os.path.join(ROOT, "profiles", "serial_step_*.md"))),
+                         ids=os.path.basename)
 def test_commands_run_committed_files_only(path):
     text = open(path).read()
     cmds = [l for l in text.splitlines() if l.startswith("rocprofv3 ")]
@@ -41,7 +42,7 @@ def test_commands_run_committed_files_only(path):
         assert "_work" not in c and "gpurun" not in c
 
 
-@pytest.mark.parametrize("path", STEP)
+@pytest.mark.parametrize("path", STEP, ids=os.path.basename)
 def test_traffic_is_the_scaled_counter_sum(path):
     kv = figures(path)
     w = os.path.basename(path)[len("gemm_step_"):-3]
