@@ -758,6 +758,36 @@ def tile_timeline(torch, w, plan, dp, b, stream):
             "position_on_chiplet_p_mod_8": round(float(np.mean(chip == pos % 8)), 4)}
 
 
+def vendor_gemm(torch, w, plan, dp, b, stream, iters, rounds=3):
+    """Context for the GEMM's roofline fraction: the vendor library's GEMM of
+    the same operands (torch.nn.functional.linear, A x W^T, hipBLASLt on
+    ROCm; a plain 2-D product, no reorder or signal) timed in rounds that
+    alternate with the signalled, reordered GEMM alone on the same box."""
+    import torch.nn.functional as F
+    dt = torch.float16 if w.dtype == "fp16" else torch.bfloat16
+    A = b.A.view(dt).reshape(w.M, w.K)
+    W = b.W.view(dt).reshape(w.N, w.K)
+    ours, theirs = [], []
+    for _ in range(rounds):
+        ours.append(time_gemm(torch, plan, dp, b, stream, iters, 3))
+        with torch.cuda.stream(stream):
+            for _ in range(3):
+                F.linear(A, W)
+            ev = [(Ev(), Ev()) for _ in range(iters)]
+            for e0, e1 in ev:
+                e0.record(stream)
+                F.linear(A, W)
+                e1.record(stream)
+        torch.cuda.synchronize()
+        theirs.append(float(np.mean([e0.elapsed_time(e1) * 1000.0 for e0, e1 in ev])))
+    flops = 2.0 * w.M * w.N * w.K
+    o, t = float(np.median(ours)), float(np.median(theirs))
+    return {"op": "torch.nn.functional.linear (A x W^T; hipBLASLt), same operands, alternating rounds",
+            "us": round(t, 2), "tflops": round(flops / t / 1e6, 2),
+            "signalled_us_same_rounds": round(o, 2), "signalled_tflops_same_rounds": round(flops / o / 1e6, 2),
+            "signalled_over_vendor_time": round(o / t, 4)}
+
+
 def cpu_baseline(w, inp, seconds, sizes, num_cus):
     """The oracle's whole path on the host: the fp64 GEMM on a seeded sample
     of output rows (sized to about `seconds`, scaled to all rows), then the
@@ -1041,6 +1071,8 @@ def main():
     t5 = table5(torch, w, inp, b, num_cus, T, s1)
     log("group-size sweep")
     sw = sweep(torch, w, inp, num_cus, b, s1, s2, max(10, args.steps // 2))
+    log("vendor GEMM")
+    vendor = vendor_gemm(torch, w, base_plan, dp_base, b, s1, max(10, args.steps // 2))
 
     # ---- every other workload -------------------------------------------------
     others = {}
@@ -1104,7 +1136,8 @@ def main():
                  "plain_static_tflops": round(flops / plain_static_us / 1e6, 2),
                  "interference_pct": round((sig_us / plain_sig_us - 1) * 100, 2),
                  "interference_vs_static_pct": round((sig_us / plain_static_us - 1) * 100, 2),
-                 "pct_peak_signaled": round(flops / sig_us / 1e6 / PEAK_TFLOPS * 100, 2)},
+                 "pct_peak_signaled": round(flops / sig_us / 1e6 / PEAK_TFLOPS * 100, 2),
+                 "vendor": vendor},
         "consumer": {"whole_buffer_us": round(cons_all_us, 2),
                      "GBps": round(cons_bytes_per_elem * n_all / cons_all_us / 1e3, 1),
                      "frac_hbm": round(cons_bytes_per_elem * n_all / cons_all_us / 1e3 / PEAK_HBM_GBS, 4),
