@@ -6,7 +6,8 @@ stores addressed in 64 bits otherwise; the consumer reads a segment with
 16-byte buffer loads when it fits 31 bits, and with 8-byte coherent loads
 otherwise. These tests run the second kind of each: a 32768 x 32768 output
 (2 GiB) and a segment of 2^30 + 37 elements. GEMM values are checked on
-seeded rows on both sides of the 2 GiB boundary against the exact product;
+seeded rows on both sides of the 2 GiB boundary against the exact product
+(and every element for having been written);
 the consumer input repeats one seeded block, so the whole output is
 compared (on the GPU) with the oracle's sum of that block, repeated.
 """
@@ -46,6 +47,8 @@ def test_signalled_gemm_output_past_2_gib():
     fo.gemm_signal_reorder(plan, dp, to_dev(A), to_dev(W), C, counters)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(counters.cpu().numpy()[:plan.P], plan.targets)
+    # every element was written: no NaN fill is left on either side of 2 GiB
+    assert not bool(torch.isnan(C.view(torch.float16)).any()), "unwritten output elements"
     rng = np.random.default_rng(43)
     rows = np.sort(np.concatenate([rng.choice(M // 2, 8, replace=False),
                                    M // 2 + rng.choice(M // 2, 8, replace=False), [M - 1]]))
