@@ -70,11 +70,11 @@ def assert_close_bits(got: np.ndarray, ref: np.ndarray, dtype: str, what: str = 
 
 
 def plan_for(w: workloads.Workload, inp: workloads.Inputs, *, num_cus=256, sizes=None, unit=None,
-             pattern=None):
+             pattern=None, group_m=4, num_xcds=8):
     pattern = pattern or w.pattern
     nd = w.num_dest if pattern in ("subtile", "subtoken") else 0
     kw = dict(dtype=w.dtype, tile_m=w.tile_m, tile_n=w.tile_n, order=w.order, num_cus=num_cus,
-              pattern=pattern, num_dest=nd,
+              group_m=group_m, num_xcds=num_xcds, pattern=pattern, num_dest=nd,
               dest_perm=inp.sigma if pattern == "subtile" else None,
               row_bucket=inp.bucket if pattern == "subtoken" else None)
     tiles = (w.M // w.tile_m) * (w.N // w.tile_n)
@@ -87,6 +87,7 @@ def plan_for(w: workloads.Workload, inp: workloads.Inputs, *, num_cus=256, sizes
     unit = unit or "waves"
     p = fo.plan_groups(w.M, w.N, w.K, sizes=sizes, unit=unit, **kw)
     o = oracle.make_plan(w.M, w.N, w.tile_m, w.tile_n, num_cus=num_cus, order=w.order,
-                         pattern=pattern, num_dest=nd, sigma=inp.sigma, bucket=inp.bucket,
+                         group_m=group_m, num_xcds=num_xcds, pattern=pattern, num_dest=nd,
+                         sigma=inp.sigma, bucket=inp.bucket,
                          sizes=sizes, unit=unit)
     return p, o

@@ -214,6 +214,47 @@ def test_random_paths(case):
     check(w, inp, plan, o)
 
 
+def dispatch_cases(n, seed=2505):
+    """Seeded random small paths over the dispatch-order parameters that the
+    GEMM evaluates per position: the grouped and XCD orders with band heights
+    1..6 (bands that do and do not divide the tile rows, one band taller than
+    the grid) and 1..12 chiplets (more than the position counters, or more
+    than the workgroups of the grid), on 2..12 modelled compute units."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for k in range(n):
+        tm, tn = [(256, 128), (256, 256), (64, 64)][int(rng.integers(3))]
+        M, N, K = tm * int(rng.integers(1, 9)), tn * int(rng.integers(1, 6)), 64 * int(rng.integers(1, 5))
+        pattern = ["tile", "subtile"][int(rng.integers(2))]
+        nd = int(rng.choice([2, 4, 8])) if pattern == "subtile" else 2
+        w = workloads.Workload(name=f"dispatch{k}", M=M, N=N, K=K, dtype=["fp16", "bf16"][int(rng.integers(2))],
+                               tile_m=tm, tile_n=tn, order=["grouped", "xcd"][int(rng.integers(2))],
+                               pattern=pattern, seed=300 + k, dist="uniform", num_dest=nd,
+                               bias=bool(rng.integers(2)), rmsnorm=False, gamma=False)
+        group_m, num_xcds = int(rng.integers(1, 7)), int(rng.integers(1, 13))
+        cus = int(rng.integers(2, 13))
+        T = -(-((M // tm) * (N // tn)) // cus)
+        sizes = _composition(rng, T, int(rng.integers(2, min(4, T) + 1))) if T > 1 else [1]
+        out.append((w, cus, sizes, group_m, num_xcds))
+    return out
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_dispatch_orders(case):
+    # the whole path (checks of test_random_paths) with the grouped and XCD
+    # dispatch orders at random band heights and chiplet counts: the GEMM
+    # computes the tile of each position itself, and must still run every
+    # tile exactly once (a tile missed leaves NaNs, a group short of its
+    # target leaves the consumer waiting) whatever the position classes
+    w, cus, sizes, group_m, num_xcds = dispatch_cases(24)[case]
+    say(f"[pipeline dispatch] {w.name} {w.M}x{w.N}x{w.K} {w.dtype} tile {w.tile_m}x{w.tile_n} {w.order} "
+        f"group_m={group_m} num_xcds={num_xcds} {w.pattern}/{w.num_dest} bias={w.bias} cus={cus} {sizes}")
+    inp = workloads.make_inputs(w)
+    plan, o = plan_for(w, inp, num_cus=cus, sizes=sizes, unit="waves", group_m=group_m, num_xcds=num_xcds)
+    np.testing.assert_array_equal(plan.order, np.array(o.order))
+    check(w, inp, plan, o)
+
+
 FULL = {
     "ar_2048x4096x4096": [(1,)],
     "rs_8192x8192x3584": [(1,) * 4, (2, 2), (1, 3)],
