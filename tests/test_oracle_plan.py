@@ -110,6 +110,26 @@ def test_grouped_order_closed_form():
     assert o[8:] == [8, 9]
 
 
+@pytest.mark.parametrize("grid", [(1, 1), (3, 2), (5, 7), (8, 32), (13, 9), (7, 1), (1, 9)])
+def test_dispatch_orders_reduce_to_plain_walks(grid):
+    # special cases with a definition of their own: bands of one row are the
+    # row-major walk; one band covering every row is the column-major walk;
+    # one chiplet is the grouped order; and for any chiplet count the
+    # positions of chiplet 0, then of chiplet 1, ... (p = x, x + X, ...) walk
+    # the grouped order from its start, each chiplet a contiguous share
+    tm, tn = grid
+    T = tm * tn
+    assert oracle.dispatch_order(tm, tn, "grouped", 1) == list(range(T))
+    for g in (tm, tm + 3):
+        assert oracle.dispatch_order(tm, tn, "grouped", g) == [(q % tm) * tn + q // tm for q in range(T)]
+    for g in (1, 2, 3, 5):
+        grouped = oracle.dispatch_order(tm, tn, "grouped", g)
+        assert oracle.dispatch_order(tm, tn, "xcd", g, 1) == grouped
+        for X in (2, 3, 8, 11, T + 2):
+            o = oracle.dispatch_order(tm, tn, "xcd", g, X)
+            assert [o[p] for x in range(X) for p in range(x, T, X)] == grouped, (g, X)
+
+
 # ---- groups and counters ----------------------------------------------------------
 
 @pytest.mark.parametrize("tiles_m,tiles_n,cus,sizes", [

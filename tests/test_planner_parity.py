@@ -90,6 +90,16 @@ def test_small_plans_match_oracle(pattern, nd, order, shape):
     _compare(p, o)
 
 
+@pytest.mark.parametrize("order", ["grouped", "xcd"])
+@pytest.mark.parametrize("group_m,num_xcds", [(1, 1), (2, 3), (5, 11), (6, 12), (40, 8)])
+def test_dispatch_parameters_match_oracle(order, group_m, num_xcds):
+    # band heights that do not divide the 13 tile rows (and one taller than
+    # the grid) and chiplet counts above the GEMM's 8 position counters
+    p, o = _both(13 * 64, 9 * 64, 64, 64, cus=10, order=order, group_m=group_m, num_xcds=num_xcds,
+                 sizes=[3, 4, 5])
+    _compare(p, o)
+
+
 def test_tile_unit_and_reserved_cus():
     p, o = _both(2048, 1024, 256, 128, cus=16, reserved=3, wg_per_cu=2, sizes=[5, 20, 39], unit="tiles")
     _compare(p, o)
