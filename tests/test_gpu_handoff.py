@@ -8,8 +8,9 @@ destination buffer), and the final consumer launch counts its finished
 workgroups into done words that a one-wave wait on the GEMM stream checks
 before the post-reorder (so the post-reorder reads complete groups and the
 next GEMM does not overwrite what a consumer still reads). These tests run
-back-to-back runs that share every buffer but their outputs, hold either
-stream back before a run, and force the bounded waits to time out from the
+back-to-back runs that share every buffer but their outputs, runs of two
+workloads on shared and on separate stream pairs, hold either stream back
+before a run, and force the bounded waits to time out from the
 host (a tiny wall-clock limit), which must end in the status bit and not in
 a hang.
 """
@@ -284,3 +285,28 @@ def test_two_plans_alternate_on_the_same_streams():
     assert int(a.status.cpu()[0]) == 0 and int(b.status.cpu()[0]) == 0
     for st, k, out in outs:
         st.check(k, out)
+
+
+def test_two_runs_at_once_on_their_own_streams():
+    # the same two workloads, each on a stream pair of its own, submitted
+    # interleaved without host synchronisation, so that their GEMMs,
+    # consumers and handoff waits run at the same time (and, with more
+    # streams than hardware queues, may share a queue with the other run's
+    # kernels): each run's handoffs see only its own counters and tags
+    torch = torch_mod()
+    say("[handoff two runs at once]")
+    a, b = Setup("rs_8192x8192x3584"), Setup("a2a_4096x7168x2048")
+    streams = {id(a): (torch.cuda.Stream(), torch.cuda.Stream()), id(b): (torch.cuda.Stream(), torch.cuda.Stream())}
+    outs = []
+    torch.cuda.synchronize()
+    for k in range(8):
+        st = a if k % 2 == 0 else b
+        out = empty16(st.w.M * st.w.N, st.w.dtype)
+        st.run(k // 2, out, *streams[id(st)])
+        outs.append((st, k // 2, out))
+    torch.cuda.synchronize()
+    assert int(a.status.cpu()[0]) == 0 and int(b.status.cpu()[0]) == 0
+    for st, k, out in outs:
+        st.check(k, out)
+    for st in (a, b):
+        np.testing.assert_array_equal(st.counters.cpu().numpy()[:st.plan.P], np.array(st.o.targets))
