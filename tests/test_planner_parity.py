@@ -187,12 +187,22 @@ def test_search_single_wave_gives_one_group():
     (dict(M=1024, N=1024, K=64, pattern="subtile", num_dest=4, dest_perm=[0, 0, 1, 2], sizes=[1]), -1),
     (dict(M=1024, N=1024, K=64, sizes=None), -1),              # search without a curve
     (dict(M=1024, N=1024, K=64, num_cus=0, sizes=[1]), -1),
+    (dict(M=1024, N=1024, K=64, order="grouped", group_m=0, sizes=[1]), -1),
+    (dict(M=1024, N=1024, K=64, order="xcd", group_m=-2, sizes=[1]), -1),
+    (dict(M=1024, N=1024, K=64, order="xcd", num_xcds=0, sizes=[1]), -1),
     (dict(M=256 * 64, N=128 * 64, K=64, num_cus=16, sizes=None, curve_bytes=[1.0], curve_us=[1.0]), -3),
 ])
 def test_plan_errors(kwargs, status):
     with pytest.raises(fo.FoError) as e:
         fo.plan_groups(**kwargs)
     assert e.value.status == status
+
+
+def test_rowmajor_order_ignores_band_and_chiplet_fields():
+    # the band height and chiplet count are read by the grouped and XCD
+    # orders only
+    p = fo.plan_groups(1024, 1024, 64, order="rowmajor", group_m=0, num_xcds=0, sizes=[1])
+    np.testing.assert_array_equal(p.order, np.arange(p.tiles))
 
 
 def test_empty_problem():
